@@ -1,0 +1,398 @@
+"""CPU oracle for Faster Flash Decoding (FFD) decode attention.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the package smoke check and the benchmark's CPU-baseline
+leg may import this module. The product path (the HIP library and its binding) never calls it.
+
+Plain, slow, obviously correct: numpy in float64, one function per step of the method, each
+citing the passage of the paper it follows. It shares no code with the HIP path.
+
+Notation (paper): ``q`` query of one head, ``k`` key, ``d`` head dimension, ``alpha = 1/sqrt(d)``;
+``k^quant`` the 2-bit thumbnail, ``k^res`` the 8-bit residual; ``m~`` the pseudo-max;
+``delta`` the top-delta margin; ``S_global`` sink tokens, ``S_local`` local tokens.
+
+Readings of the paper taken where it is silent or ambiguous (each is listed in the design notes):
+
+* Quantizer (App. A): one scale per token per KV head over its ``d`` channels, ``s = M / 1.5`` with
+  ``M = max_i |k_i|``; nearest level of ``{-1.5, -0.5, 0.5, 1.5}``; a tie at a bin edge goes to the
+  upper level; ``M = 0`` gives code 2 (level +0.5) and a zero reconstruction.
+* Residual (Sec. 3.1 "8-bit residual"): an int8 ``r`` on the shared step ``s / 254`` so that
+  ``k^quant + k^res = (s)(level + r/254) = M n / 381`` with ``n = rint(381 k / M)`` (ties to even)
+  and ``r = n - 254 c + 381`` in ``[-127, 127]``.
+* All scores (scan, pseudo-max, block score, refined logits) carry the ``1/sqrt(d)`` of Eq. 1.
+* The pseudo-max (Alg. 1; Eq. 3) is taken over thumbnail scores of the first ``n_sink`` tokens and
+  the last ``n_local`` tokens of the sequence.
+* A block is tokens ``[B*j, min(B*j + B, L))``; only valid tokens enter its score and the softmax.
+* Masks are per query head; a KV head's residual/values are read for the union over its group.
+* An empty selection or an empty sequence gives output 0 and ``lse = -inf``.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+# App. A: the 4-level symmetric mid-rise codebook; code c in {0,1,2,3} stands for level c - 1.5.
+CODEBOOK = np.array([-1.5, -0.5, 0.5, 1.5], dtype=np.float64)
+RESID_STEPS = 254          # residual step is s / 254 (Sec. 3.1 8-bit residual reading)
+FULL_LEVELS = 381          # 1.5 * 254: k^quant + k^res = M * n / 381
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Decode bf16 bit patterns (uint16) into float64 values (exact)."""
+    u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    with np.errstate(invalid="ignore"):
+        return u32.view(np.float32).astype(np.float64)
+
+
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bf16 bit patterns (nearest, ties to even), via float32."""
+    u = np.ascontiguousarray(np.asarray(x, dtype=np.float32)).view(np.uint32)
+    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+# ------------------------------------------------------------------------------------------------
+# Q1/Q2. Key decomposition k -> {k^quant, k^res} (Sec. 3.1; App. A formulation).
+# ------------------------------------------------------------------------------------------------
+
+def quantize_keys(K: np.ndarray):
+    """Thumbnail codes, absmax and residual of every key vector (App. A; Sec. 3.1).
+
+    ``K``: float64 ``[..., d]`` of bf16-exact values. Returns ``codes`` (int64 in 0..3),
+    ``M`` (float64 ``[...]``, the per-vector absmax) and ``resid`` (int64 in -127..127).
+
+    The nearest-level rule of App. A is applied with exact comparisons: ``x/s`` against the bin
+    edges -1, 0, +1 is ``3k`` against ``-2M, 0, 2M``; a tie goes to the upper level.
+    """
+    K = np.asarray(K, dtype=np.float64)
+    M = np.max(np.abs(K), axis=-1)
+    Mx = M[..., None]
+    codes = np.where(3.0 * K >= 2.0 * Mx, 3,
+                     np.where(K >= 0.0, 2,
+                              np.where(3.0 * K >= -2.0 * Mx, 1, 0))).astype(np.int64)
+    zero = Mx == 0.0
+    codes = np.where(zero, 2, codes)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        n = np.rint(FULL_LEVELS * K / Mx)          # round half to even
+    n = np.where(zero, 0.0, n).astype(np.int64)
+    resid = np.where(zero, 0, n - RESID_STEPS * codes + FULL_LEVELS).astype(np.int64)
+    return codes, M, resid
+
+
+def thumbnail(codes: np.ndarray, M: np.ndarray) -> np.ndarray:
+    """Dequantized thumbnail ``k^quant = x_q * s`` with ``s = M / 1.5`` (App. A reconstruction)."""
+    s = np.asarray(M, dtype=np.float64)[..., None] / 1.5
+    return CODEBOOK[codes] * s
+
+
+def residual_part(resid: np.ndarray, M: np.ndarray) -> np.ndarray:
+    """The residual's contribution ``k^res = s * r / 254`` (Sec. 3.1 reading; Eq. 4's second term)."""
+    s = np.asarray(M, dtype=np.float64)[..., None] / 1.5
+    return s * (np.asarray(resid, dtype=np.float64) / RESID_STEPS)
+
+
+# ------------------------------------------------------------------------------------------------
+# S1. Thumbnail scan (Alg. 1 top-delta loop; Sec. 3.3 step 2), scaled by 1/sqrt(d) (Eq. 1).
+# ------------------------------------------------------------------------------------------------
+
+def scan_scores(q: np.ndarray, codes: np.ndarray, M: np.ndarray, alpha: float) -> np.ndarray:
+    """``s_hat[h, t] = alpha * q_h . k^quant_t`` for every head of the group and every token."""
+    return alpha * (np.asarray(q, dtype=np.float64) @ thumbnail(codes, M).T)
+
+
+# ------------------------------------------------------------------------------------------------
+# S2. Pseudo-max over sink and local tokens (Alg. 1 pseudo-max lines; Sec. 3.2 Eq. 3).
+# ------------------------------------------------------------------------------------------------
+
+def pseudo_max_tokens(L: int, n_sink: int, n_local: int) -> np.ndarray:
+    """Indices of ``S_global`` (first ``n_sink``) and ``S_local`` (last ``n_local``), clipped to L."""
+    sink = np.arange(0, min(n_sink, L))
+    local = np.arange(max(0, L - n_local), L)
+    return np.union1d(sink, local).astype(np.int64)
+
+
+def pseudo_max(s_hat: np.ndarray, L: int, n_sink: int, n_local: int) -> np.ndarray:
+    """``m~_h = max(max_{S_global} s_hat, max_{S_local} s_hat)`` per head; ``-inf`` if both are empty."""
+    idx = pseudo_max_tokens(L, n_sink, n_local)
+    if idx.size == 0:
+        return np.full(s_hat.shape[0], -np.inf)
+    return np.max(s_hat[:, idx], axis=1)
+
+
+# ------------------------------------------------------------------------------------------------
+# S3. Block score and top-delta decision (Alg. 1 selection; Eq. 1 with m replaced by m~).
+# ------------------------------------------------------------------------------------------------
+
+def block_scores(s_hat: np.ndarray, L: int, block: int) -> np.ndarray:
+    """``sigma[h, j] = max`` of ``s_hat`` over the valid tokens of block ``j``."""
+    nblk = -(-L // block)
+    out = np.full((s_hat.shape[0], nblk), -np.inf)
+    for j in range(nblk):
+        out[:, j] = np.max(s_hat[:, j * block:min(j * block + block, L)], axis=1)
+    return out
+
+
+def select_blocks(sigma: np.ndarray, m_tilde: np.ndarray, delta: float) -> np.ndarray:
+    """Keep block ``j`` for head ``h`` iff ``sigma[h, j] >= m~_h - delta`` (inclusive, Eq. 1)."""
+    return sigma >= (m_tilde[:, None] - delta)
+
+
+# ------------------------------------------------------------------------------------------------
+# S4. Refinement with scan reuse (Alg. 1 refinement; Sec. 3.3 Eq. 4).
+# ------------------------------------------------------------------------------------------------
+
+def refined_logits(q, codes, M, resid, alpha):
+    """``s_final = (q . k^quant + q . k^res) / sqrt(d)``: the scan term plus the residual term."""
+    q = np.asarray(q, dtype=np.float64)
+    return alpha * (q @ thumbnail(codes, M).T + q @ residual_part(resid, M).T)
+
+
+# ------------------------------------------------------------------------------------------------
+# S5. Sparse softmax . V over the selected tokens (Alg. 1 output line).
+# ------------------------------------------------------------------------------------------------
+
+def softmax_attend(z: np.ndarray, V: np.ndarray):
+    """Softmax of ``z`` over its tokens times ``V``; returns ``(o, lse)``. Empty -> ``(0, -inf)``."""
+    V = np.asarray(V, dtype=np.float64)
+    if z.size == 0:
+        return np.zeros(V.shape[-1]), -np.inf
+    m = np.max(z)
+    p = np.exp(z - m)
+    l = np.sum(p)
+    return (p @ V) / l, m + np.log(l)
+
+
+def token_mask_from_blocks(keep_blocks: np.ndarray, L: int, block: int) -> np.ndarray:
+    """Expand a per-block keep vector to the valid tokens ``t < L``."""
+    return np.repeat(np.asarray(keep_blocks, dtype=bool), block)[:L]
+
+
+# ------------------------------------------------------------------------------------------------
+# S6. Exact dense attention (the comparator's definition) over the exact bf16 keys.
+# ------------------------------------------------------------------------------------------------
+
+def dense_attention(q, K, V, L, alpha):
+    """``softmax(alpha q K^T) V`` over tokens ``t < L`` for every head of the group."""
+    q = np.asarray(q, dtype=np.float64)
+    outs, lses = [], []
+    for h in range(q.shape[0]):
+        z = alpha * (np.asarray(K[:L], dtype=np.float64) @ q[h])
+        o, lse = softmax_attend(z, V[:L])
+        outs.append(o)
+        lses.append(lse)
+    return np.stack(outs), np.array(lses)
+
+
+# ------------------------------------------------------------------------------------------------
+# Split-K partials and their log-sum-exp merge (flash-decoding split along the sequence, Sec. 2).
+# ------------------------------------------------------------------------------------------------
+
+def partial_state(z, V):
+    """One split's ``(m, l, acc)``: running max, sum of ``exp(z - m)``, unnormalised output."""
+    if z.size == 0:
+        return -np.inf, 0.0, np.zeros(np.asarray(V).shape[-1])
+    m = np.max(z)
+    p = np.exp(z - m)
+    return m, np.sum(p), p @ np.asarray(V, dtype=np.float64)
+
+
+def lse_merge(states):
+    """Merge split states: ``M* = max m_s``, ``l* = sum e^{m_s - M*} l_s``, ``o = sum e^{m_s-M*} acc_s / l*``."""
+    ms = np.array([s[0] for s in states], dtype=np.float64)
+    if ms.size == 0 or not np.isfinite(ms).any():
+        return np.zeros_like(states[0][2]) if states else None, -np.inf
+    Mx = np.max(ms)
+    w = np.where(np.isfinite(ms), np.exp(ms - Mx), 0.0)
+    l = sum(wi * s[1] for wi, s in zip(w, states))
+    acc = sum(wi * s[2] for wi, s in zip(w, states))
+    return acc / l, Mx + np.log(l)
+
+
+# ------------------------------------------------------------------------------------------------
+# The whole decode step for one (sequence, KV head) group, and for a batch.
+# ------------------------------------------------------------------------------------------------
+
+def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None):
+    """FFD decode for the ``G`` query heads ``q [G, d]`` sharing keys ``K [Lcap, d]``, values ``V``.
+
+    Follows Alg. 1 in order: quantize, pseudo-max, top-delta selection, refinement, softmax . V.
+    When ``keep`` (bool ``[G, nblk]``) is given, attention runs on that mask instead of the
+    oracle's own selection (used to compare outputs given the GPU's mask).
+    """
+    codes, M, resid = quantize_keys(K[:L])
+    s_hat = scan_scores(q, codes, M, alpha)
+    m_tilde = pseudo_max(s_hat, L, n_sink, n_local)
+    sigma = block_scores(s_hat, L, block)
+    own_keep = select_blocks(sigma, m_tilde, delta)
+    use = own_keep if keep is None else np.asarray(keep, dtype=bool)[:, :sigma.shape[1]]
+    z_all = refined_logits(q, codes, M, resid, alpha)
+    outs, lses = [], []
+    for h in range(q.shape[0]):
+        tok = token_mask_from_blocks(use[h], L, block)
+        o, lse = softmax_attend(z_all[h, :L][tok], np.asarray(V[:L], dtype=np.float64)[tok])
+        outs.append(o)
+        lses.append(lse)
+    return dict(out=np.stack(outs), lse=np.array(lses), keep=own_keep, sigma=sigma,
+                m_tilde=m_tilde, s_hat=s_hat)
+
+
+def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, block=64,
+                 softmax_scale=None, keep=None, heads=None):
+    """FFD decode for a batch. Inputs are bf16 bit patterns ``q [B,Hq,d]``, ``k, v [B,Hkv,Lcap,d]``.
+
+    Returns float64 ``out [B,Hq,d]``, ``lse [B,Hq]``, the per-head block mask ``keep [B,Hq,nblk]``
+    (blocks at or beyond a sequence's end are False), ``sigma`` and ``m_tilde``.
+    ``heads`` optionally restricts work to a list of ``(b, kvh)`` pairs (others left as NaN).
+    """
+    B, Hq, d = q_bits.shape
+    Hkv, Lcap = k_bits.shape[1], k_bits.shape[2]
+    G = Hq // Hkv
+    alpha = 1.0 / np.sqrt(d) if not softmax_scale else float(softmax_scale)
+    nblk = -(-Lcap // block)
+    out = np.full((B, Hq, d), np.nan)
+    lse = np.full((B, Hq), np.nan)
+    mask = np.zeros((B, Hq, nblk), dtype=bool)
+    sigma = np.full((B, Hq, nblk), -np.inf)
+    m_tilde = np.full((B, Hq), np.nan)
+    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hkv)]
+    for b, h in pairs:
+        L = int(seq_lens[b])
+        sl = slice(h * G, (h + 1) * G)
+        q = bf16_to_f64(q_bits[b, sl])
+        if L == 0:
+            out[b, sl] = 0.0
+            lse[b, sl] = -np.inf
+            m_tilde[b, sl] = -np.inf
+            continue
+        K = bf16_to_f64(k_bits[b, h, :L])
+        V = bf16_to_f64(v_bits[b, h, :L])
+        kb = None if keep is None else np.asarray(keep[b, sl], dtype=bool)
+        r = decode_group(q, K, V, L, delta=delta, n_sink=n_sink, n_local=n_local, block=block,
+                         alpha=alpha, keep=kb)
+        nb = r["sigma"].shape[1]
+        out[b, sl] = r["out"]
+        lse[b, sl] = r["lse"]
+        mask[b, sl, :nb] = r["keep"]
+        sigma[b, sl, :nb] = r["sigma"]
+        m_tilde[b, sl] = r["m_tilde"]
+    return dict(out=out, lse=lse, keep=mask, sigma=sigma, m_tilde=m_tilde)
+
+
+def dense_batch(q_bits, k_bits, v_bits, seq_lens, *, softmax_scale=None, heads=None):
+    """Exact dense attention over bf16 keys/values for a batch (the dense baseline's definition)."""
+    B, Hq, d = q_bits.shape
+    Hkv = k_bits.shape[1]
+    G = Hq // Hkv
+    alpha = 1.0 / np.sqrt(d) if not softmax_scale else float(softmax_scale)
+    out = np.full((B, Hq, d), np.nan)
+    lse = np.full((B, Hq), np.nan)
+    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hkv)]
+    for b, h in pairs:
+        L = int(seq_lens[b])
+        sl = slice(h * G, (h + 1) * G)
+        o, l = dense_attention(bf16_to_f64(q_bits[b, sl]), bf16_to_f64(k_bits[b, h, :L]),
+                               bf16_to_f64(v_bits[b, h, :L]), L, alpha)
+        out[b, sl] = o
+        lse[b, sl] = l
+    return dict(out=out, lse=lse)
+
+
+def near_threshold(sigma, m_tilde, delta, band=1e-3):
+    """Blocks whose score lies within ``band`` of the threshold ``m~ - delta`` (reported apart)."""
+    thr = np.asarray(m_tilde)[..., None] - delta
+    with np.errstate(invalid="ignore"):
+        return np.isfinite(sigma) & (np.abs(sigma - thr) < band)
+
+
+# ------------------------------------------------------------------------------------------------
+# Storage layouts of the quantized copy (this implementation's format; the paper fixes none).
+# They are written out independently of the HIP code, from the format's definition:
+#
+#  codes  uint32 [B, Hkv, Lcap/32, 64, 4]. In slab S (tokens 32S..32S+31), lane l = n + 16g and
+#         word w = 2*tt + cc hold the 16 codes of token 32S + 16tt + n for dims 64cc + 16g + e,
+#         e = 4k + b, at bits 8b + 2k.
+#  absmax bf16 [B, Hkv, Lcap/64, 16, 4]. Element [j, n, t4] is M of token 64j + 16t4 + n.
+#  resid  int8 [B, Hkv, Lcap/16, 2, 64, 16]. Element [T, cc, n + 16g, e] is the residual of
+#         token 16T + n at dim 64cc + 16g + e.
+# ------------------------------------------------------------------------------------------------
+
+def pack_codes(codes: np.ndarray) -> np.ndarray:
+    """Pack ``codes [Lcap, 128]`` (0..3) into the ``[Lcap/32, 64, 4]`` uint32 layout above."""
+    Lcap = codes.shape[0]
+    out = np.zeros((Lcap // 32, 64, 4), dtype=np.uint32)
+    c = np.asarray(codes, dtype=np.uint32)
+    for S in range(Lcap // 32):
+        for g in range(4):
+            for n in range(16):
+                lane = n + 16 * g
+                for tt in range(2):
+                    t = 32 * S + 16 * tt + n
+                    for cc in range(2):
+                        word = 0
+                        for e in range(16):
+                            k, b = divmod(e, 4)
+                            word |= int(c[t, 64 * cc + 16 * g + e]) << (8 * b + 2 * k)
+                        out[S, lane, 2 * tt + cc] = word
+    return out
+
+
+def unpack_codes(packed: np.ndarray, Lcap: int) -> np.ndarray:
+    """Inverse of :func:`pack_codes`."""
+    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 32, 64, 4)
+    codes = np.zeros((Lcap, 128), dtype=np.int64)
+    for S in range(Lcap // 32):
+        for g in range(4):
+            for n in range(16):
+                for tt in range(2):
+                    for cc in range(2):
+                        word = int(packed[S, n + 16 * g, 2 * tt + cc])
+                        for e in range(16):
+                            k, b = divmod(e, 4)
+                            codes[32 * S + 16 * tt + n, 64 * cc + 16 * g + e] = (word >> (8 * b + 2 * k)) & 3
+    return codes
+
+
+def pack_codes_fast(codes: np.ndarray) -> np.ndarray:
+    """Vectorised :func:`pack_codes` (checked equal to the loop form on small inputs)."""
+    Lcap = codes.shape[0]
+    c = np.asarray(codes, dtype=np.uint32).reshape(Lcap // 32, 2, 16, 2, 4, 4, 4)  # S,tt,n,cc,g,k,b
+    c = c.transpose(0, 4, 2, 1, 3, 5, 6)                                            # S,g,n,tt,cc,k,b
+    shift = (8 * np.arange(4)[None, :] + 2 * np.arange(4)[:, None]).astype(np.uint32)  # [k, b]
+    words = np.bitwise_or.reduce((c << shift).reshape(*c.shape[:5], 16), axis=-1)
+    return words.reshape(Lcap // 32, 64, 4).astype(np.uint32)
+
+
+def pack_absmax(M_bits: np.ndarray) -> np.ndarray:
+    """Permute per-token absmax bits ``[Lcap]`` into the ``[Lcap/64, 16, 4]`` layout above."""
+    Lcap = M_bits.shape[0]
+    return np.asarray(M_bits).reshape(Lcap // 64, 4, 16).transpose(0, 2, 1).copy()
+
+
+def pack_resid(resid: np.ndarray) -> np.ndarray:
+    """Tile residuals ``[Lcap, 128]`` into the ``[Lcap/16, 2, 64, 16]`` int8 layout above."""
+    Lcap = resid.shape[0]
+    r = np.asarray(resid, dtype=np.int8).reshape(Lcap // 16, 16, 2, 4, 16)  # T,n,cc,g,e
+    return r.transpose(0, 2, 3, 1, 4).reshape(Lcap // 16, 2, 64, 16).copy()
+
+
+def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = None):
+    """Oracle for the quantization pass: packed ``(codes, absmax_bits, resid)`` for ``[B,Hkv,Lcap,128]``.
+
+    Only tokens in ``[t_begin, t_end)`` are defined; the others are returned as zero.
+    """
+    B, Hkv, Lcap, d = k_bits.shape
+    t_end = Lcap if t_end is None else t_end
+    codes = np.zeros((B, Hkv, Lcap // 32, 64, 4), dtype=np.uint32)
+    absmax = np.zeros((B, Hkv, Lcap // 64, 16, 4), dtype=np.uint16)
+    resid = np.zeros((B, Hkv, Lcap // 16, 2, 64, 16), dtype=np.int8)
+    for b in range(B):
+        for h in range(Hkv):
+            K = bf16_to_f64(k_bits[b, h])
+            c, M, r = quantize_keys(K)
+            live = np.zeros(Lcap, dtype=bool)
+            live[t_begin:t_end] = True
+            c = np.where(live[:, None], c, 0)
+            r = np.where(live[:, None], r, 0)
+            Mb = np.where(live, f64_to_bf16_bits(M), 0).astype(np.uint16)
+            codes[b, h] = pack_codes_fast(c)
+            absmax[b, h] = pack_absmax(Mb)
+            resid[b, h] = pack_resid(r)
+    return codes, absmax, resid
