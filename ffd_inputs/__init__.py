@@ -4,12 +4,13 @@ This module is shared by the CPU oracle and by the GPU path. It holds none of th
 arithmetic: it only draws queries, keys and values, plants structure (heavy blocks, an attention
 sink, a recent window), and rounds float32 draws to bfloat16 bit patterns.
 
-Recipe (one ``numpy.random.default_rng(seed)`` stream, fixed draw order):
+Recipe:
 
-1. ragged workloads draw the per-sequence lengths first;
-2. ``q ~ N(0, 1)`` of shape ``[B, Hq, D]``, rounded to bf16;
-3. for each sequence ``b`` and each KV head ``kvh`` (row-major order): ``K ~ N(0, 1)`` and
-   ``V ~ N(0, 1)`` of shape ``[Lcap, D]``, then that pair's structure draws.
+1. ``numpy.random.default_rng(seed)``: ragged workloads draw the per-sequence lengths first, then
+   ``q ~ N(0, 1)`` of shape ``[B, Hq, D]``, rounded to bf16;
+2. each sequence ``b`` and KV head ``kvh`` has its own stream ``default_rng([seed, b, kvh])``:
+   ``K ~ N(0, 1)`` and ``V ~ N(0, 1)`` of shape ``[Lcap, D]``, then that pair's structure draws.
+   Pairs are independent, so they are generated in parallel threads.
 
 Structure. A planted direction per ``(b, kvh)`` is ``u = sqrt(D) * qbar / |qbar|`` where ``qbar``
 is the mean of the group's bf16 queries; ``|u| = sqrt(D)`` is the norm of a typical N(0,1) key.
@@ -23,6 +24,8 @@ Arrays are returned as ``uint16`` bf16 bit patterns.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -41,8 +44,12 @@ POISON_VALUE = 64.0
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bf16 (ties to even) and return the bit patterns."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -129,30 +136,35 @@ def generate(*, name, seed, B, Hq, Hkv, Lcap, seq_lens, heavy_fn, sink_fn=lambda
     q = f32_to_bf16_bits(rng.standard_normal((B, Hq, D), dtype=np.float32))
     k = np.empty((B, Hkv, Lcap, D), dtype=np.uint16)
     v = np.empty((B, Hkv, Lcap, D), dtype=np.uint16)
-    heavy, sinks = {}, np.zeros(B, dtype=bool)
-    for b in range(B):
+    sinks = np.array([bool(sink_fn(b)) for b in range(B)], dtype=bool)
+
+    def one_pair(b, h):
+        prng = np.random.default_rng([seed, b, h])
         L = int(seq_lens[b])
-        sinks[b] = bool(sink_fn(b))
-        for h in range(Hkv):
-            kf = rng.standard_normal((Lcap, D), dtype=np.float32)
-            vf = rng.standard_normal((Lcap, D), dtype=np.float32)
-            u = _planted_direction(q[b, h * G:(h + 1) * G])
-            blocks = list(heavy_fn(rng, b, h, L))
-            heavy[(b, h)] = blocks
-            for j in blocks:
-                lo, hi = j * block, min(j * block + block, L)
-                noise = rng.standard_normal((hi - lo, D), dtype=np.float32)
-                kf[lo:hi] = HEAVY_AMPLITUDE * u + PLANT_NOISE_STD * noise
-            if sinks[b] and L > 0:
-                kf[0] = HEAVY_AMPLITUDE * u + PLANT_NOISE_STD * rng.standard_normal(D, dtype=np.float32)
-            if recent_tokens and L > 0:
-                lo = max(0, L - recent_tokens)
-                noise = rng.standard_normal((L - lo, D), dtype=np.float32)
-                kf[lo:L] = RECENT_AMPLITUDE * u + PLANT_NOISE_STD * noise
-            kf[L:] = POISON_KEY_SCALE * u
-            vf[L:] = POISON_VALUE
-            k[b, h] = f32_to_bf16_bits(kf)
-            v[b, h] = f32_to_bf16_bits(vf)
+        kf = prng.standard_normal((Lcap, D), dtype=np.float32)
+        vf = prng.standard_normal((Lcap, D), dtype=np.float32)
+        u = _planted_direction(q[b, h * G:(h + 1) * G])
+        blocks = list(heavy_fn(prng, b, h, L))
+        for j in blocks:
+            lo, hi = j * block, min(j * block + block, L)
+            noise = prng.standard_normal((hi - lo, D), dtype=np.float32)
+            kf[lo:hi] = HEAVY_AMPLITUDE * u + PLANT_NOISE_STD * noise
+        if sinks[b] and L > 0:
+            kf[0] = HEAVY_AMPLITUDE * u + PLANT_NOISE_STD * prng.standard_normal(D, dtype=np.float32)
+        if recent_tokens and L > 0:
+            lo = max(0, L - recent_tokens)
+            noise = prng.standard_normal((L - lo, D), dtype=np.float32)
+            kf[lo:L] = RECENT_AMPLITUDE * u + PLANT_NOISE_STD * noise
+        kf[L:] = POISON_KEY_SCALE * u
+        vf[L:] = POISON_VALUE
+        k[b, h] = f32_to_bf16_bits(kf)
+        v[b, h] = f32_to_bf16_bits(vf)
+        return (b, h), blocks
+
+    pairs = [(b, h) for b in range(B) for h in range(Hkv)]
+    workers = max(1, min(len(pairs), 16, os.cpu_count() or 1))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        heavy = dict(ex.map(lambda bh: one_pair(*bh), pairs))
     return Case(name=name, seed=seed, B=B, Hq=Hq, Hkv=Hkv, D=D, Lcap=Lcap, block=block,
                 seq_lens=seq_lens, q=q, k=k, v=v, n_sink=n_sink, n_local=n_local,
                 deltas=tuple(deltas), heavy_blocks=heavy, sink=sinks, recent_tokens=recent_tokens)
@@ -204,7 +216,7 @@ def workload(n: int, seed: int | None = None) -> Case:
     if n == 5:
         Lcap, B = 131072, 16
         rng = np.random.default_rng(seed)
-        lens = rng.integers(8192, 131072, size=B, endpoint=True)
+        lens = rng.integers(8192, 131072, size=B, endpoint=True)   # drawn before q
 
         def heavy5(rng, b, h, L):
             if b % 2:

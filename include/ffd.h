@@ -1,0 +1,131 @@
+/*
+ * ffd.h — C ABI of the Faster Flash Decoding (FFD) decode-attention library for AMD MI355X (gfx950).
+ *
+ * One decode step of grouped-query attention for a batch of sequences:
+ *
+ *   ffd_quantize_keys           split each key into a 2-bit thumbnail and an 8-bit residual
+ *                               (Sec. 3.1; App. A formulation; Fig. 2 "K quantization").
+ *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), 2-bit scan and
+ *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement that reuses
+ *                               the scan dot products (Eq. 4), online-softmax attention over the kept
+ *                               blocks, split along the sequence and merged by log-sum-exp
+ *                               (flash-decoding, Sec. 2 and Sec. 3.3).
+ *   ffd_dense_decode_attention  exact dense decode attention over the bf16 cache (the dense
+ *                               comparator of Sec. 4.2), same split-and-merge scheme.
+ *
+ * Conventions for every entry point
+ *  - Tensor arguments are DEVICE pointers to contiguous row-major buffers owned by the caller.
+ *    The library never allocates, frees or retains them, never synchronises the host, and keeps no
+ *    mutable global state. Calls are asynchronous on `stream`; outputs are valid once it completes.
+ *  - bf16 tensors are passed as `const void*` holding IEEE bfloat16 bit patterns.
+ *  - Shapes: B sequences, Hq query heads, Hkv KV heads (Hq % Hkv == 0, G = Hq / Hkv in {1,2,4,8};
+ *    query head h reads KV head h / G), head dimension D == 128, cache capacity Lcap tokens
+ *    (a multiple of 64), KV block of 64 tokens.
+ *  - seq_lens is a device int32 [B]; sequence b holds tokens [0, seq_lens[b]). Values are clamped
+ *    to [0, Lcap] on the device (no host synchronisation to check them).
+ *  - Pointers must be 16-byte aligned. Argument checks run before any launch; on failure nothing is
+ *    enqueued and an ffd_status error is returned. A failed launch returns FFD_ERR_HIP.
+ *
+ * Quantized-key storage (this library's format; the paper fixes none). Per (b, kvh):
+ *  - codes  uint32 [Lcap/32][64][4]: slab S = tokens 32S..32S+31; lane l = n + 16g and word
+ *           w = 2tt + cc hold the 16 codes of token 32S + 16tt + n for dims 64cc + 16g + e,
+ *           e = 4k + b, at bits 8b + 2k. Code c in {0,1,2,3} stands for level c - 1.5.
+ *  - absmax bf16 [Lcap/64][16][4]: element [j][n][t4] = M = max_i |k_i| of token 64j + 16t4 + n.
+ *  - resid  int8 [Lcap/16][2][64][16]: element [T][cc][n + 16g][e] is the residual of token 16T + n
+ *           at dim 64cc + 16g + e.
+ *  The reconstruction is k ~= M * n / 381 with n = 254 c + r - 381 (thumbnail step M/1.5,
+ *  residual step M/(1.5*254)); the thumbnail alone is k^quant = (c - 1.5) * M / 1.5.
+ */
+#ifndef FFD_H
+#define FFD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FFD_OK = 0,
+    FFD_ERR_INVALID_ARGUMENT = 1,    /* null/misaligned pointer, bad shape, bad delta, bad range   */
+    FFD_ERR_UNSUPPORTED = 2,         /* valid but not implemented: D != 128, block != 64, G > 8    */
+    FFD_ERR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes < ffd_workspace_bytes(...)                 */
+    FFD_ERR_HIP = 4                  /* a HIP launch failed (hipGetLastError after the launch)     */
+} ffd_status;
+
+#define FFD_HEAD_DIM 128
+#define FFD_BLOCK 64
+#define FFD_MAX_SPLITS 1024
+
+/*
+ * Key quantization (Sec. 3.1: k -> {k^quant, k^res}; App. A: symmetric mid-rise 2-bit codebook
+ * {-1.5,-0.5,0.5,1.5}, s = max|k|/1.5, nearest level; ties at bin edges go to the upper level).
+ * Residual: r = rint(381 k / M) - 254 c + 381 in [-127, 127] (round half to even); M = 0 gives
+ * code 2 and residual 0.
+ *
+ *   k         bf16  [B, Hkv, Lcap, D]      keys (read)
+ *   k_codes   uint32 codes layout above    (written for tokens [t_begin, t_end) only)
+ *   k_absmax  bf16  absmax layout above    (written for tokens [t_begin, t_end) only)
+ *   k_resid   int8  resid layout above     (written for tokens [t_begin, t_end) only)
+ *   0 <= t_begin <= t_end <= Lcap. Tokens outside the range are left untouched, so appending one
+ *   decode-step token is t_begin = L, t_end = L + 1.
+ */
+int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resid,
+                      int B, int Hkv, int Lcap, int D, int t_begin, int t_end, hipStream_t stream);
+
+/*
+ * FFD decode attention (Alg. 1 with Eq. 1-4), one query per head.
+ *
+ *   q            bf16  [B, Hq, D]
+ *   k_codes, k_absmax, k_resid   quantized keys (from ffd_quantize_keys)
+ *   v            bf16  [B, Hkv, Lcap, D]
+ *   seq_lens     int32 [B] (device)
+ *   block_size   must be 64
+ *   delta        top-delta margin >= 0 (+inf keeps every block); a block j is kept for head h iff
+ *                max over its valid tokens of the thumbnail score >= m~_h - delta, where
+ *                m~_h is the max thumbnail score over tokens [0, n_sink) U [L - n_local, L).
+ *                All scores carry softmax_scale. With n_sink = n_local = 0, m~ = -inf and every
+ *                block is kept.
+ *   num_splits   splits of each sequence's blocks (1..FFD_MAX_SPLITS), or 0 for automatic.
+ *   softmax_scale  > 0, or 0 for 1/sqrt(D).
+ *   out          bf16  [B, Hq, D]  softmax(z over kept tokens) . V, z the refined logits;
+ *                                   0 for a head with no kept token (empty sequence).
+ *   lse          float [B, Hq] or NULL: ln sum exp(z) over kept tokens (-inf if none).
+ *   block_mask   uint8 [B, Hq, Lcap/64] or NULL: 1 iff head h kept block j; 0 at/after the end.
+ *   workspace    device scratch of at least ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)
+ *                bytes; contents need no initialisation and are clobbered.
+ */
+int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax,
+                         const void* k_resid, const void* v, const int32_t* seq_lens,
+                         int B, int Hq, int Hkv, int Lcap, int D, int block_size, float delta,
+                         int n_sink, int n_local, int num_splits, float softmax_scale,
+                         void* out, float* lse, uint8_t* block_mask,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Exact dense decode attention over bf16 keys and values (the FlashAttention-2 comparator of
+ * Sec. 4.2): out = softmax(softmax_scale * q K^T) V over tokens [0, seq_lens[b]).
+ * Arguments as above; k is bf16 [B, Hkv, Lcap, D].
+ */
+int ffd_dense_decode_attention(const void* q, const void* k, const void* v, const int32_t* seq_lens,
+                               int B, int Hq, int Hkv, int Lcap, int D, int num_splits,
+                               float softmax_scale, void* out, float* lse,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Number of splits a call with this num_splits (0 = automatic) will use. 0 on invalid input. */
+int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
+
+/* Workspace bytes needed by either attention entry point for these arguments:
+ * B * Hq * S * (D + 2) * 4 with S = ffd_resolve_splits(...). 0 on invalid input. */
+size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
+
+/* Static, human-readable name of a status code. */
+const char* ffd_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FFD_H */

@@ -1,0 +1,189 @@
+"""Thin Python binding of libffd.so (ctypes). Argument marshalling only: every step of the decode
+path runs in the library's HIP kernels. PyTorch supplies device memory and the current stream.
+
+If the library is not built or cannot be loaded, every call raises ``FfdLibraryError``; there is
+no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libffd.so")
+
+HEAD_DIM = 128
+BLOCK = 64
+MAX_SPLITS = 1024
+STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
+          3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
+
+EXPORTS = ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
+           "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_status_string")
+
+
+class FfdLibraryError(RuntimeError):
+    """libffd.so is missing or failed to load."""
+
+
+class FfdError(RuntimeError):
+    """A library call returned an error status."""
+
+    def __init__(self, fn: str, status: int, detail: str):
+        super().__init__(f"{fn} -> {detail} ({status})")
+        self.status = status
+
+
+_lib = None
+P, I, F, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """Load libffd.so (once) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise FfdLibraryError(f"{LIB_PATH} is not built; run paper_2609_00097_amd/build.py")
+    try:
+        so = ctypes.CDLL(LIB_PATH)
+    except OSError as e:
+        raise FfdLibraryError(f"cannot load {LIB_PATH}: {e}") from e
+    so.ffd_quantize_keys.argtypes = [P, P, P, P, I, I, I, I, I, I, P]
+    so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, I, I, F,
+                                        P, P, P, P, SZ, P]
+    so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
+    so.ffd_resolve_splits.argtypes = [I, I, I, I]
+    so.ffd_workspace_bytes.argtypes = [I, I, I, I, I, I]
+    so.ffd_workspace_bytes.restype = SZ
+    so.ffd_status_string.argtypes = [I]
+    so.ffd_status_string.restype = ctypes.c_char_p
+    for name in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
+                 "ffd_resolve_splits"):
+        getattr(so, name).restype = I
+    _lib = so
+    return so
+
+
+def _check(fn: str, st: int) -> None:
+    if st != 0:
+        raise FfdError(fn, st, lib().ffd_status_string(st).decode())
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _need(t, name, dtype, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
+    return lib().ffd_resolve_splits(B, Hkv, Lcap, num_splits)
+
+
+def workspace_bytes(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
+    return lib().ffd_workspace_bytes(B, Hq, Hkv, Lcap, HEAD_DIM, num_splits)
+
+
+def quantized_shapes(B: int, Hkv: int, Lcap: int):
+    """Shapes of (codes int32, absmax bf16, resid int8) for a cache of capacity Lcap."""
+    return ((B, Hkv, Lcap // 32, 64, 4), (B, Hkv, Lcap // 64, 16, 4),
+            (B, Hkv, Lcap // 16, 2, 64, 16))
+
+
+def empty_quantized(B: int, Hkv: int, Lcap: int, device):
+    sc, sa, sr = quantized_shapes(B, Hkv, Lcap)
+    return (torch.empty(sc, dtype=torch.int32, device=device),
+            torch.empty(sa, dtype=torch.bfloat16, device=device),
+            torch.empty(sr, dtype=torch.int8, device=device))
+
+
+def quantize_keys(k: torch.Tensor, t_begin: int = 0, t_end: int | None = None, out=None):
+    """Split bf16 keys ``[B, Hkv, Lcap, 128]`` into (codes, absmax, resid) for ``[t_begin, t_end)``."""
+    if k.dim() != 4:
+        raise ValueError("k must be [B, Hkv, Lcap, 128]")
+    B, Hkv, Lcap, D = k.shape
+    _need(k, "k", torch.bfloat16)
+    t_end = Lcap if t_end is None else t_end
+    codes, absmax, resid = out if out is not None else empty_quantized(B, Hkv, Lcap, k.device)
+    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
+                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
+        _need(t, nm, dt, sh)
+    _check("ffd_quantize_keys", lib().ffd_quantize_keys(
+        _ptr(k), _ptr(codes), _ptr(absmax), _ptr(resid), B, Hkv, Lcap, D, t_begin, t_end,
+        _stream(k.device)))
+    return codes, absmax, resid
+
+
+def _attn_outputs(q, B, Hq, Lcap, want_lse, want_mask, out, lse, mask):
+    out = torch.empty((B, Hq, HEAD_DIM), dtype=torch.bfloat16, device=q.device) if out is None else out
+    if want_lse and lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    if want_mask and mask is None:
+        mask = torch.empty((B, Hq, Lcap // BLOCK), dtype=torch.uint8, device=q.device)
+    return out, lse, mask
+
+
+def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_sink: int = 64,
+                     n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
+                     return_lse: bool = True, return_mask: bool = False, workspace=None,
+                     out=None, lse=None, mask=None):
+    """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested)."""
+    B, Hq, D = q.shape
+    Hkv, Lcap = v.shape[1], v.shape[2]
+    _need(q, "q", torch.bfloat16)
+    _need(v, "v", torch.bfloat16, (B, Hkv, Lcap, D))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
+                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
+        _need(t, nm, dt, sh)
+    out, lse, mask = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None,
+                                   return_mask or mask is not None, out, lse, mask)
+    nbytes = workspace_bytes(B, Hq, Hkv, Lcap, num_splits)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+    _check("ffd_decode_attention", lib().ffd_decode_attention(
+        _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
+        D, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
+        _ptr(lse), _ptr(mask), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(q.device)))
+    return out, lse, mask
+
+
+def dense_decode_attention(q, k, v, seq_lens, *, num_splits: int = 0, softmax_scale: float = 0.0,
+                           return_lse: bool = True, workspace=None, out=None, lse=None):
+    """Exact dense decode attention. Returns ``(out, lse)``."""
+    B, Hq, D = q.shape
+    Hkv, Lcap = k.shape[1], k.shape[2]
+    _need(q, "q", torch.bfloat16)
+    _need(k, "k", torch.bfloat16, (B, Hkv, Lcap, D))
+    _need(v, "v", torch.bfloat16, (B, Hkv, Lcap, D))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    out, lse, _ = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None, False, out, lse, None)
+    nbytes = workspace_bytes(B, Hq, Hkv, Lcap, num_splits)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+    _check("ffd_dense_decode_attention", lib().ffd_dense_decode_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap, D, num_splits,
+        float(softmax_scale), _ptr(out), _ptr(lse), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(q.device)))
+    return out, lse
+
+
+def default_scale() -> float:
+    return 1.0 / math.sqrt(HEAD_DIM)

@@ -1,0 +1,144 @@
+"""ffd_decode_attention on the GPU: block masks and outputs against the oracle (Alg. 1; Eq. 1-4).
+
+Masks must be bit-exact except blocks whose score lies within 1e-3 of the threshold (counted and
+printed); outputs and lse are compared with the oracle's attention on the GPU's own mask.
+"""
+import numpy as np
+import pytest
+import torch
+
+import ffd_inputs as I
+from oracle import ffd_oracle as O
+from tests.gpu_util import Uploaded, bf16_to_f64, check_close, check_lse, compare_ffd
+
+pytestmark = pytest.mark.gpu
+
+
+def _quant(up):
+    from paper_2609_00097_amd import ffd
+    return ffd.quantize_keys(up.k)
+
+
+def _ffd(up, qk, delta, n_sink=None, n_local=None, num_splits=0):
+    from paper_2609_00097_amd import ffd
+    c = up.case
+    out, lse, mask = ffd.decode_attention(
+        up.q, *qk, up.v, up.seq_lens, delta=delta,
+        n_sink=c.n_sink if n_sink is None else n_sink, n_local=c.n_local if n_local is None else n_local,
+        num_splits=num_splits, return_lse=True, return_mask=True)
+    torch.cuda.synchronize()
+    return out, lse, mask
+
+
+@pytest.mark.parametrize("delta", [3.0, 5.0, 7.0])
+def test_workload1_delta_sweep(delta):
+    c = I.workload(1)
+    print(f"case {c.name} seed {c.seed} delta {delta}", flush=True)
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), delta)
+    near, flipped = compare_ffd(c, delta, out, lse, mask)
+    print(f"near-threshold blocks {near}, flipped among them {flipped}; kept {int(mask.sum())}")
+
+
+def test_workload2():
+    c = I.workload(2)
+    print(f"case {c.name} seed {c.seed}", flush=True)
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), 5.0)
+    near, flipped = compare_ffd(c, 5.0, out, lse, mask)
+    print(f"near-threshold blocks {near}, flipped {flipped}; kept {int(mask.sum())}")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 4), (8, 2), (16, 2)])
+@pytest.mark.parametrize("lens", [(1,), (63, 64, 65), (320, 1000, 4097)])
+def test_gqa_ratios_and_ragged_lengths(Hq, Hkv, lens):
+    c = I.small_case(seed=7 * len(lens) + Hq + 3 * Hkv, B=len(lens), Hq=Hq, Hkv=Hkv, seq_lens=lens)
+    print(f"case ffd Hq={Hq} Hkv={Hkv} lens={lens}", flush=True)
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), 5.0)
+    compare_ffd(c, 5.0, out, lse, mask)
+
+
+@pytest.mark.parametrize("n_sink,n_local", [(0, 0), (0, 64), (64, 0), (1, 1), (5000, 10)])
+def test_window_sizes(n_sink, n_local):
+    c = I.small_case(seed=41, B=2, Hq=8, Hkv=2, seq_lens=(2500, 700), Lcap=2560)
+    print(f"case windows {n_sink},{n_local}", flush=True)
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), 5.0, n_sink, n_local)
+    compare_ffd(c, 5.0, out, lse, mask, n_sink=n_sink, n_local=n_local)
+    if n_sink == 0 and n_local == 0:
+        assert mask.cpu().numpy()[0, :, :40].all()    # m~ = -inf keeps every block
+
+
+def test_delta_zero_and_infinite():
+    c = I.small_case(seed=43, B=2, Hq=8, Hkv=2, seq_lens=(1500, 4000))
+    up = Uploaded(c)
+    qk = _quant(up)
+    out0, lse0, mask0 = _ffd(up, qk, 0.0)
+    compare_ffd(c, 0.0, out0, lse0, mask0)
+    outi, lsei, maski = _ffd(up, qk, float("inf"))
+    m = maski.cpu().numpy()
+    for b, L in enumerate(c.seq_lens):
+        nb = -(-int(L) // 64)
+        assert m[b, :, :nb].all() and not m[b, :, nb:].any()
+    # delta = inf is dense attention on the 2+8 reconstruction (pinned in the oracle tests)
+    compare_ffd(c, float("inf"), outi, lsei, maski)
+
+
+def test_zero_keys_and_short_sequences():
+    """All-zero key tokens (M = 0), sequences shorter than the windows, and an empty sequence."""
+    c = I.small_case(seed=47, B=4, Hq=8, Hkv=2, seq_lens=(300, 1, 0, 129), Lcap=320)
+    c.k[0, :, 10:80] = 0
+    c.k[3, 1, :] = 0
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), 5.0)
+    compare_ffd(c, 5.0, out, lse, mask)
+    o = bf16_to_f64(out)
+    assert np.all(o[2] == 0) and np.all(np.isneginf(lse.cpu().numpy()[2]))
+    assert not mask.cpu().numpy()[2].any()
+
+
+def test_split_count_invariance():
+    c = I.small_case(seed=53, B=2, Hq=8, Hkv=2, seq_lens=(6000, 2222), heavy_frac=0.05)
+    up = Uploaded(c)
+    qk = _quant(up)
+    ref_out, ref_lse, ref_mask = _ffd(up, qk, 5.0, num_splits=1)
+    for s in (2, 7, 64, 0):
+        out, lse, mask = _ffd(up, qk, 5.0, num_splits=s)
+        assert torch.equal(mask, ref_mask)
+        np.testing.assert_allclose(bf16_to_f64(out), bf16_to_f64(ref_out), rtol=1e-2, atol=2e-3)
+        np.testing.assert_allclose(lse.cpu().numpy(), ref_lse.cpu().numpy(), rtol=0, atol=1e-4)
+    compare_ffd(c, 5.0, ref_out, ref_lse, ref_mask)
+
+
+def test_argument_errors_return_status_without_launch():
+    from paper_2609_00097_amd import ffd
+    c = I.small_case(seed=1, B=1, Hq=8, Hkv=2, seq_lens=(100,))
+    up = Uploaded(c)
+    qk = _quant(up)
+    with pytest.raises(ffd.FfdError) as e:
+        ffd.decode_attention(up.q, *qk, up.v, up.seq_lens, delta=-1.0)
+    assert e.value.status == 1
+    ws = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ffd.FfdError) as e:
+        ffd.decode_attention(up.q, *qk, up.v, up.seq_lens, delta=5.0, workspace=ws)
+    assert e.value.status == 3
+
+
+@pytest.mark.parametrize("wl,heads", [(3, [(0, 0), (1, 3), (3, 7)]), (4, [(0, 0), (0, 5)]),
+                                      (5, [(0, 0), (1, 2), (6, 5), (15, 7)])])
+def test_full_size_workloads_sampled(wl, heads):
+    """Workloads 3-5 at full size in the benchmark's launch configuration (automatic splits);
+    masks and outputs against the oracle on sampled (sequence, KV head) pairs."""
+    c = I.workload(wl)
+    print(f"case {c.name} seed {c.seed} pairs {heads}", flush=True)
+    up = Uploaded(c)
+    qk = _quant(up)
+    out, lse, mask = _ffd(up, qk, 5.0)
+    near, flipped = compare_ffd(c, 5.0, out, lse, mask, heads=heads)
+    keep = mask.cpu().numpy()
+    print(f"near-threshold blocks {near}, flipped {flipped}; kept fraction {keep.mean():.4f}")
+    # no head anywhere ends with an empty selection (the pseudo-max's own block always passes)
+    for b, L in enumerate(c.seq_lens):
+        if L > 0:
+            assert keep[b].any(axis=-1).all()
