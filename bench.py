@@ -1,0 +1,270 @@
+"""Benchmark of one FFD decode step on one MI355X, with the dense flash-decode baseline beside it.
+
+A step is one ffd_decode_attention call (pseudo-max, 2-bit scan, top-delta decision, refinement,
+online softmax . V, split merge) over one batch of synthetic inputs already resident in HBM.
+Every timed step is preceded by an untimed 1 GiB read of another buffer that evicts the 256 MB
+Infinity Cache and the L2 with clean lines, so the step streams from HBM as it would between the
+layers of a real decode. (A write-based flush would leave up to 256 MB of dirty lines whose
+write-back then competes with the measured step; a plain 134 MB stream measures ~25 us after a
+read flush and ~48 us after a write flush on MI355X.)
+
+Prints ONE JSON line. ``value`` is microseconds per decode step (lower is better); effective HBM
+bandwidth is the algorithmic bytes of the step (scan of every valid token's codes and absmax,
+residual + values of the tokens in blocks kept by any head of a KV group, queries, outputs and
+split partials) divided by the step time.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, AMD published
+SCAN_BYTES_PER_TOKEN = 32 + 2         # 2-bit codes for 128 dims + bf16 absmax
+GATHER_BYTES_PER_TOKEN = 128 + 256    # int8 residual + bf16 values
+DENSE_BYTES_PER_TOKEN = 256 + 256     # bf16 keys + values
+METRIC = ("µs/decode step + effective HBM TB/s at 128K ctx; speedup vs dense flash-decode")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = 128K x 4 sequences)")
+    ap.add_argument("--delta", type=float, default=5.0)
+    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--flush-mib", type=int, default=1024)
+    ap.add_argument("--dense-steps", type=int, default=20)
+    ap.add_argument("--sweep-deltas", default="3,7", help="extra deltas timed (10 steps each)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + timed FFD steps only (for rocprofv3 runs)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(case, mask, S):
+    """Bytes one FFD step must move, counted from the measured per-head block mask."""
+    G, D = case.G, case.D
+    scan = 0
+    gather_tokens = 0
+    for b in range(case.B):
+        L = int(case.seq_lens[b])
+        nb = -(-L // 64)
+        scan += SCAN_BYTES_PER_TOKEN * L * case.Hkv
+        for h in range(case.Hkv):
+            union = mask[b, h * G:(h + 1) * G, :nb].any(axis=0)
+            toks = union.astype(np.int64) * 64
+            if nb and union[nb - 1]:
+                toks[nb - 1] = L - 64 * (nb - 1)
+            gather_tokens += int(toks.sum())
+    gather = GATHER_BYTES_PER_TOKEN * gather_tokens
+    io = case.B * case.Hq * (2 * D + 2 * D + 4)                  # q in, out, lse
+    partials = 2 * case.B * case.Hq * S * (D + 2) * 4              # written, then read by the merge
+    return dict(scan=scan, gather=gather, io=io, partials=partials,
+                total=scan + gather + io + partials, gather_tokens=gather_tokens)
+
+
+def dense_bytes(case, S):
+    tok = int(np.sum(case.seq_lens)) * case.Hkv
+    return DENSE_BYTES_PER_TOKEN * tok + case.B * case.Hq * (4 * case.D + 4) + \
+        2 * case.B * case.Hq * S * (case.D + 2) * 4
+
+
+def time_steps(fn, steps, warmup, flush, stream):
+    import torch
+    for _ in range(warmup):
+        flush.zero_()
+        fn()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        flush.zero_()
+        starts[i].record(stream)
+        fn()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    return ms, wall
+
+
+def cpu_baseline(case, delta, budget_s):
+    """The oracle's decode step (given the quantized keys) on host cores, over a bounded sample of
+    (sequence, KV head) pairs, scaled to the whole step."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import ffd_oracle as O
+    pairs = [(b, h) for b in range(case.B) for h in range(case.Hkv)]
+    alpha = 1.0 / math.sqrt(case.D)
+    G = case.G
+    spent, done, tokens = 0.0, 0, 0
+    for b, h in pairs:
+        L = int(case.seq_lens[b])
+        q = O.bf16_to_f64(case.q[b, h * G:(h + 1) * G])
+        K = O.bf16_to_f64(case.k[b, h, :L])
+        V = O.bf16_to_f64(case.v[b, h, :L])
+        codes, M, resid = O.quantize_keys(K)            # cache write, not part of the step
+        t0 = time.perf_counter()
+        O.decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=case.n_sink,
+                                 n_local=case.n_local, block=64, alpha=alpha)
+        spent += time.perf_counter() - t0
+        done += 1
+        tokens += L
+        if spent >= budget_s:
+            break
+    total_tokens = int(np.sum(case.seq_lens)) * case.Hkv
+    us_step = spent / tokens * total_tokens * 1e6
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": round(us_step, 1), "unit": "us/step", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {len(pairs)} (sequence, KV head) pairs of the workload, "
+                      f"{tokens} tokens, {spent:.1f} s, scaled by token count to the whole step; "
+                      f"float64 numpy, host affinity {len(os.sched_getaffinity(0))} CPUs"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(each (sequence, KV head) pair is independent; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import ffd_inputs as I
+    from paper_2609_00097_amd import ffd
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    case = I.workload(args.workload)
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = up(case.q), up(case.k), up(case.v)
+    lens = torch.from_numpy(case.seq_lens.astype(np.int32)).to(dev)
+    S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, args.splits)
+    ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev)
+    codes, absmax, resid = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
+    flush_buf = torch.ones((args.flush_mib << 20) // 4, dtype=torch.int32, device=dev)
+
+    class _ReadFlush:
+        """Evicts the caches by reading flush_buf (the reduction writes one scalar)."""
+        def zero_(self):
+            torch.sum(flush_buf)
+    flush = _ReadFlush()
+
+    # cache write (once per prefill; reported, not part of the step)
+    qs, qe = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flush.zero_()
+    qs.record(stream)
+    ffd.quantize_keys(k, out=(codes, absmax, resid))
+    qe.record(stream)
+    torch.cuda.synchronize()
+    quant_ms = qs.elapsed_time(qe)
+
+    out = torch.empty((case.B, case.Hq, case.D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((case.B, case.Hq), dtype=torch.float32, device=dev)
+    mask = torch.empty((case.B, case.Hq, case.Lcap // 64), dtype=torch.uint8, device=dev)
+
+    def ffd_step(delta=args.delta):
+        ffd.decode_attention(q, codes, absmax, resid, v, lens, delta=delta, n_sink=case.n_sink,
+                             n_local=case.n_local, num_splits=args.splits, workspace=ws, out=out,
+                             lse=lse)
+
+    # the measured mask gives the algorithmic bytes (mask output off in the timed steps)
+    def mask_for(delta):
+        ffd.decode_attention(q, codes, absmax, resid, v, lens, delta=delta, n_sink=case.n_sink,
+                             n_local=case.n_local, num_splits=args.splits, workspace=ws, out=out,
+                             lse=lse, mask=mask)
+        torch.cuda.synchronize()
+        return mask.cpu().numpy().astype(bool)
+
+    keep = mask_for(args.delta)
+    nbytes = algorithmic_bytes(case, keep, S)
+
+    ms, wall = time_steps(ffd_step, args.steps, args.warmup, flush, stream)
+    if args.profile_only:
+        print(json.dumps({"profile_only": True, "ffd_us_mean": float(ms.mean() * 1e3)}))
+        return
+    us = float(ms.mean() * 1e3)
+    tbps = nbytes["total"] / (us * 1e-6) / 1e12
+
+    # dense flash-decode baseline, same protocol
+    dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev)
+
+    def dense_step():
+        ffd.dense_decode_attention(q, k, v, lens, num_splits=args.splits, workspace=dws, out=out,
+                                   lse=lse)
+    dms, _ = time_steps(dense_step, args.dense_steps, 3, flush, stream)
+    dense_us = float(dms.mean() * 1e3)
+    dbytes = dense_bytes(case, S)
+
+    sweep = {}
+    for d in [float(x) for x in args.sweep_deltas.split(",") if x.strip()]:
+        kd = mask_for(d)
+        bd = algorithmic_bytes(case, kd, S)
+        sms, _ = time_steps(lambda: ffd_step(d), 10, 2, flush, stream)
+        su = float(sms.mean() * 1e3)
+        sweep[str(d)] = {"us": round(su, 2), "tbps": round(bd["total"] / (su * 1e-6) / 1e12, 3),
+                         "keep_head_blocks": round(float(kd.mean()), 5),
+                         "speedup_vs_dense": round(dense_us / su, 2)}
+
+    G = case.G
+    valid_blocks = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel()
+                                   for b in range(case.B)])
+    union_frac = nbytes["gather_tokens"] / float(np.sum(case.seq_lens) * case.Hkv)
+    line = {
+        "metric": METRIC,
+        "value": round(us, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8+f32",
+        "data": "synthetic",
+        "config": {"workload": case.name, "batch": case.B, "context": int(case.Lcap),
+                   "q_heads": case.Hq, "kv_heads": case.Hkv, "head_dim": case.D, "kv_block": 64,
+                   "delta": args.delta, "n_sink": case.n_sink, "n_local": case.n_local,
+                   "num_splits": S, "io": "q/v/out bf16, k as 2-bit codes + int8 residual",
+                   "cache_flush_between_steps_mib": args.flush_mib, "cache_flush": "read"},
+        "effective_tbps": round(tbps, 3),
+        "hbm_peak_frac": round(tbps * 1e3 / HBM_PEAK_GBPS, 4),
+        "bytes_per_step": nbytes,
+        "us_p10_p50_p90": [round(float(np.percentile(ms, p)) * 1e3, 2) for p in (10, 50, 90)],
+        "keep_head_blocks": round(float(valid_blocks.mean()), 5),
+        "keep_union_tokens": round(union_frac, 5),
+        "dense_us": round(dense_us, 2),
+        "dense_tbps": round(dbytes / (dense_us * 1e-6) / 1e12, 3),
+        "speedup_vs_dense": round(dense_us / us, 2),
+        "delta_sweep": sweep,
+        "quantize_cache_us": round(quant_ms * 1e3, 1),
+        "wall_s_timed_region": round(wall, 3),
+        "roofline": {"bound": "hbm", "achieved": round(nbytes["total"] / (us * 1e-6) / 1e9, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(nbytes["total"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "traffic": None,
+                     "kernel": "ffd_decode_kernel (one launch per step, split merge fused), HIP events"},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(case, args.delta, args.cpu_seconds)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

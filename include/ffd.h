@@ -27,10 +27,10 @@
  *    enqueued and an ffd_status error is returned. A failed launch returns FFD_ERR_HIP.
  *
  * Quantized-key storage (this library's format; the paper fixes none). Per (b, kvh):
- *  - codes  uint32 [Lcap/32][64][4]: slab S = tokens 32S..32S+31; lane l = n + 16g and word
- *           w = 2tt + cc hold the 16 codes of token 32S + 16tt + n for dims 64cc + 16g + e,
+ *  - codes  uint32 [Lcap/64][64][8]: block j = tokens 64j..64j+63; lane l = n + 16g and word
+ *           w = 2*t4 + cc hold the 16 codes of token 64j + 16*t4 + n for dims 64cc + 16g + e,
  *           e = 4k + b, at bits 8b + 2k. Code c in {0,1,2,3} stands for level c - 1.5.
- *  - absmax bf16 [Lcap/64][16][4]: element [j][n][t4] = M = max_i |k_i| of token 64j + 16t4 + n.
+ *  - absmax bf16 [Lcap/64][16][4]: element [j][n][t4] = M = max_i |k_i| of token 64j + 16*t4 + n.
  *  - resid  int8 [Lcap/16][2][64][16]: element [T][cc][n + 16g][e] is the residual of token 16T + n
  *           at dim 64cc + 16g + e.
  *  The reconstruction is k ~= M * n / 381 with n = 254 c + r - 381 (thumbnail step M/1.5,
@@ -95,7 +95,8 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
  *   lse          float [B, Hq] or NULL: ln sum exp(z) over kept tokens (-inf if none).
  *   block_mask   uint8 [B, Hq, Lcap/64] or NULL: 1 iff head h kept block j; 0 at/after the end.
  *   workspace    device scratch of at least ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)
- *                bytes; contents need no initialisation and are clobbered.
+ *                bytes holding the split partials; it needs no initialisation and is clobbered.
+ *                Calls that overlap in time (different streams) need separate workspaces.
  */
 int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax,
                          const void* k_resid, const void* v, const int32_t* seq_lens,
@@ -118,7 +119,8 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
 int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
 /* Workspace bytes needed by either attention entry point for these arguments:
- * B * Hq * S * (D + 2) * 4 with S = ffd_resolve_splits(...). 0 on invalid input. */
+ * B * Hq * S * (D + 2) * 4 (fp32 partials m, l, acc) with S = ffd_resolve_splits(...).
+ * 0 on invalid input. */
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
 
 /* Static, human-readable name of a status code. */

@@ -218,6 +218,14 @@ def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None)
     oracle's own selection (used to compare outputs given the GPU's mask).
     """
     codes, M, resid = quantize_keys(K[:L])
+    return decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=n_sink,
+                                  n_local=n_local, block=block, alpha=alpha, keep=keep)
+
+
+def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, block, alpha,
+                           keep=None):
+    """The decode step of :func:`decode_group` given the already quantized keys (Alg. 1 from the
+    pseudo-max on; the quantization happens when the cache is written, Fig. 2)."""
     s_hat = scan_scores(q, codes, M, alpha)
     m_tilde = pseudo_max(s_hat, L, n_sink, n_local)
     sigma = block_scores(s_hat, L, block)
@@ -306,58 +314,57 @@ def near_threshold(sigma, m_tilde, delta, band=1e-3):
 # Storage layouts of the quantized copy (this implementation's format; the paper fixes none).
 # They are written out independently of the HIP code, from the format's definition:
 #
-#  codes  uint32 [B, Hkv, Lcap/32, 64, 4]. In slab S (tokens 32S..32S+31), lane l = n + 16g and
-#         word w = 2*tt + cc hold the 16 codes of token 32S + 16tt + n for dims 64cc + 16g + e,
+#  codes  uint32 [B, Hkv, Lcap/64, 64, 8]. In block j (tokens 64j..64j+63), lane l = n + 16g and
+#         word w = 2*t4 + cc hold the 16 codes of token 64j + 16*t4 + n for dims 64cc + 16g + e,
 #         e = 4k + b, at bits 8b + 2k.
-#  absmax bf16 [B, Hkv, Lcap/64, 16, 4]. Element [j, n, t4] is M of token 64j + 16t4 + n.
+#  absmax bf16 [B, Hkv, Lcap/64, 16, 4]. Element [j, n, t4] is M of token 64j + 16*t4 + n.
 #  resid  int8 [B, Hkv, Lcap/16, 2, 64, 16]. Element [T, cc, n + 16g, e] is the residual of
 #         token 16T + n at dim 64cc + 16g + e.
 # ------------------------------------------------------------------------------------------------
 
 def pack_codes(codes: np.ndarray) -> np.ndarray:
-    """Pack ``codes [Lcap, 128]`` (0..3) into the ``[Lcap/32, 64, 4]`` uint32 layout above."""
+    """Pack ``codes [Lcap, 128]`` (0..3) into the ``[Lcap/64, 64, 8]`` uint32 layout above."""
     Lcap = codes.shape[0]
-    out = np.zeros((Lcap // 32, 64, 4), dtype=np.uint32)
+    out = np.zeros((Lcap // 64, 64, 8), dtype=np.uint32)
     c = np.asarray(codes, dtype=np.uint32)
-    for S in range(Lcap // 32):
+    for j in range(Lcap // 64):
         for g in range(4):
             for n in range(16):
-                lane = n + 16 * g
-                for tt in range(2):
-                    t = 32 * S + 16 * tt + n
+                for t4 in range(4):
+                    t = 64 * j + 16 * t4 + n
                     for cc in range(2):
                         word = 0
                         for e in range(16):
                             k, b = divmod(e, 4)
                             word |= int(c[t, 64 * cc + 16 * g + e]) << (8 * b + 2 * k)
-                        out[S, lane, 2 * tt + cc] = word
+                        out[j, n + 16 * g, 2 * t4 + cc] = word
     return out
 
 
 def unpack_codes(packed: np.ndarray, Lcap: int) -> np.ndarray:
     """Inverse of :func:`pack_codes`."""
-    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 32, 64, 4)
+    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 64, 64, 8)
     codes = np.zeros((Lcap, 128), dtype=np.int64)
-    for S in range(Lcap // 32):
+    for j in range(Lcap // 64):
         for g in range(4):
             for n in range(16):
-                for tt in range(2):
+                for t4 in range(4):
                     for cc in range(2):
-                        word = int(packed[S, n + 16 * g, 2 * tt + cc])
+                        word = int(packed[j, n + 16 * g, 2 * t4 + cc])
                         for e in range(16):
                             k, b = divmod(e, 4)
-                            codes[32 * S + 16 * tt + n, 64 * cc + 16 * g + e] = (word >> (8 * b + 2 * k)) & 3
+                            codes[64 * j + 16 * t4 + n, 64 * cc + 16 * g + e] = (word >> (8 * b + 2 * k)) & 3
     return codes
 
 
 def pack_codes_fast(codes: np.ndarray) -> np.ndarray:
     """Vectorised :func:`pack_codes` (checked equal to the loop form on small inputs)."""
     Lcap = codes.shape[0]
-    c = np.asarray(codes, dtype=np.uint32).reshape(Lcap // 32, 2, 16, 2, 4, 4, 4)  # S,tt,n,cc,g,k,b
-    c = c.transpose(0, 4, 2, 1, 3, 5, 6)                                            # S,g,n,tt,cc,k,b
+    c = np.asarray(codes, dtype=np.uint32).reshape(Lcap // 64, 4, 16, 2, 4, 4, 4)  # j,t4,n,cc,g,k,b
+    c = c.transpose(0, 4, 2, 1, 3, 5, 6)                                           # j,g,n,t4,cc,k,b
     shift = (8 * np.arange(4)[None, :] + 2 * np.arange(4)[:, None]).astype(np.uint32)  # [k, b]
     words = np.bitwise_or.reduce((c << shift).reshape(*c.shape[:5], 16), axis=-1)
-    return words.reshape(Lcap // 32, 64, 4).astype(np.uint32)
+    return words.reshape(Lcap // 64, 64, 8).astype(np.uint32)
 
 
 def pack_absmax(M_bits: np.ndarray) -> np.ndarray:
@@ -380,7 +387,7 @@ def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = Non
     """
     B, Hkv, Lcap, d = k_bits.shape
     t_end = Lcap if t_end is None else t_end
-    codes = np.zeros((B, Hkv, Lcap // 32, 64, 4), dtype=np.uint32)
+    codes = np.zeros((B, Hkv, Lcap // 64, 64, 8), dtype=np.uint32)
     absmax = np.zeros((B, Hkv, Lcap // 64, 16, 4), dtype=np.uint16)
     resid = np.zeros((B, Hkv, Lcap // 16, 2, 64, 16), dtype=np.int8)
     for b in range(B):

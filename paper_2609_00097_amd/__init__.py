@@ -4,5 +4,5 @@ The compute path is ``libffd.so`` (HIP kernels behind a C ABI, declared in ``inc
 ``ffd`` is its ctypes binding.
 """
 from .ffd import (BLOCK, HEAD_DIM, FfdError, FfdLibraryError, decode_attention,  # noqa: F401
-                  dense_decode_attention, empty_quantized, lib, quantize_keys, quantized_shapes,
+                  dense_decode_attention, empty_quantized, lib, new_workspace, quantize_keys, quantized_shapes,
                   resolve_splits, workspace_bytes)

@@ -44,11 +44,14 @@ int launch_status() {
     return e == hipSuccess ? FFD_OK : FFD_ERR_HIP;
 }
 
+// Workspace: split partials m [B,Hq,S], l [B,Hq,S], acc [B,Hq,S,D] (fp32).
 struct Partials {
     float* m;
     float* l;
     float* acc;
 };
+
+size_t partials_bytes(int B, int Hq, int S, int D) { return (size_t)B * Hq * S * (D + 2) * sizeof(float); }
 
 Partials carve(void* ws, int B, int Hq, int S) {
     const size_t rows = (size_t)B * Hq * S;
@@ -88,7 +91,7 @@ size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_spli
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
     const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
     if (S <= 0) return 0;
-    return (size_t)B * Hq * S * (D + 2) * sizeof(float);
+    return partials_bytes(B, Hq, S, D);
 }
 
 const char* ffd_status_string(int status) {
@@ -136,8 +139,8 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
     const Partials P = carve(workspace, B, Hq, S);
     DecodeArgs a{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
                  static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid),
-                 static_cast<const uint16_t*>(v), seq_lens, P.m, P.l, P.acc, block_mask,
-                 Hq, Hkv, Lcap, G, S, delta, scale, n_sink, n_local};
+                 static_cast<const uint16_t*>(v), seq_lens, P.m, P.l, P.acc, block_mask, Hq, Hkv,
+                 Lcap, G, S, delta, scale, n_sink, n_local};
     const dim3 grid((unsigned)S, (unsigned)Hkv, (unsigned)B);
     if (G <= 4)
         hipLaunchKernelGGL(ffd_decode_kernel<1>, grid, dim3(kThreads), 0, stream, a);
@@ -145,8 +148,8 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
         hipLaunchKernelGGL(ffd_decode_kernel<2>, grid, dim3(kThreads), 0, stream, a);
     st = launch_status();
     if (st != FFD_OK) return st;
-    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kD), 0, stream, P.m, P.l, P.acc, S,
-                       static_cast<uint16_t*>(out), lse);
+    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, P.m, P.l,
+                       P.acc, S, static_cast<uint16_t*>(out), lse);
     return launch_status();
 }
 
@@ -171,8 +174,8 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
         hipLaunchKernelGGL(dense_decode_kernel<2>, grid, dim3(kThreads), 0, stream, a);
     st = launch_status();
     if (st != FFD_OK) return st;
-    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kD), 0, stream, P.m, P.l, P.acc, S,
-                       static_cast<uint16_t*>(out), lse);
+    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, P.m, P.l,
+                       P.acc, S, static_cast<uint16_t*>(out), lse);
     return launch_status();
 }
 

@@ -1,11 +1,12 @@
 // Dense flash-decode attention for gfx950 (the exact comparator): softmax(alpha q K^T) V over all
 // tokens of each sequence, split along the sequence and merged by log-sum-exp.
 //
-// Mapping. One workgroup (4 waves) serves one (sequence, KV head, split); waves take the split's
-// 64-token blocks with stride 4. QK^T runs on v_mfma_f32_16x16x32_bf16 with the queries as the A
-// operand (head h of a 4-head tile on row 4h, other rows zero) and 16 tokens per tile as B: lane
-// (g, n) loads token n's dims 32g..32g+31 (64 contiguous bytes), so its output register 0 is head
-// g's score for token n. PV runs on the VALU in fp32 (see pv_update).
+// Mapping. A workgroup (4 waves) serves one (sequence, KV head, split); wave w owns the 16-token
+// tile w of every 64-token block and keeps its own online-softmax state. QK^T runs on
+// v_mfma_f32_16x16x32_bf16 with the queries as the A operand (head h of a 4-head tile on row 4h,
+// other rows zero) and the tile's keys as B: lane (g, n) loads token n's dims 32g..32g+31 (64
+// contiguous bytes), so its output register 0 is head g's score for token n. PV runs on the VALU
+// in fp32. The next block's key and value tiles are requested before the current one is used.
 #include "ffd_device.h"
 #include "ffd_kernels.h"
 
@@ -15,14 +16,28 @@ namespace {
 
 template <int NT>
 struct DenseLds {
-    WaveP<NT> wp[kWaves];
+    TileP<NT> tp[kWaves];
     EpilogueLds<NT> epi;
 };
+
+struct KTile {
+    uint4 k[4];
+};
+
+// Key row `tok`, clamped to last_row (a valid row): the score of a token past the end is masked to
+// -inf by the caller. The loads are unconditional so the compiler can count them.
+__device__ __forceinline__ KTile load_ktile(const uint16_t* k_bh, int tok, int last_row, int g) {
+    KTile r;
+    const uint4* kp = reinterpret_cast<const uint4*>(k_bh + (size_t)min(tok, last_row) * kD + 32 * g);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) r.k[ks] = kp[ks];
+    return r;
+}
 
 }  // namespace
 
 template <int NT>
-__global__ __launch_bounds__(kThreads) void dense_decode_kernel(DenseArgs a) {
+__global__ __launch_bounds__(kThreads, NT == 1 ? 4 : 2) void dense_decode_kernel(DenseArgs a) {
     __shared__ DenseLds<NT> sm;
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -35,6 +50,12 @@ __global__ __launch_bounds__(kThreads) void dense_decode_kernel(DenseArgs a) {
     const int jb = min(s * bps, nblk), je = min(jb + bps, nblk);
     const uint16_t* k_bh = a.k + bh * (size_t)a.Lcap * kD;
     const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
+
+    // First block's tiles before the setup. Rows are clamped to the last valid row, so look-ahead
+    // past the split never leaves the sequence; the real index decides what is valid.
+    const int last_row = max(L, 1) - 1;
+    KTile kc = load_ktile(k_bh, 64 * jb + 16 * wave + n, last_row, g);
+    VTile vc = load_vtile(v_bh, 64 * jb + 16 * wave, last_row, lane);
 
     // A operand: lane (m = n, g), k-step ks holds q[head][32g + 8ks .. +8] on rows m = 4h.
     v8bf Aq[NT][4];
@@ -57,50 +78,28 @@ __global__ __launch_bounds__(kThreads) void dense_decode_kernel(DenseArgs a) {
     float m_run[NT], l_part[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) { m_run[t] = -INFINITY; l_part[t] = 0.f; }
-    WaveP<NT>& wp = sm.wp[wave];
+    TileP<NT>& tp = sm.tp[wave];
 
-    for (int j = jb + wave; j < je; j += kWaves) {
-        float z[NT][4];
-#pragma unroll
-        for (int T4 = 0; T4 < 4; ++T4) {
-            const int tok = 64 * j + 16 * T4 + n;
-            const uint4* kp = reinterpret_cast<const uint4*>(k_bh + (size_t)tok * kD + 32 * g);
-            uint4 kk[4];
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kk[ks] = tok < L ? kp[ks] : make_uint4(0, 0, 0, 0);
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks)
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Aq[t][ks], __builtin_bit_cast(v8bf, kk[ks]),
-                                                                  acc, 0, 0, 0);
-                z[t][T4] = tok < L ? acc.x * a.scale : -INFINITY;
-            }
-        }
+    for (int j = jb; j < je; ++j) {
+        const int tok = 64 * j + 16 * wave + n;
+        const KTile kn = load_ktile(k_bh, 64 * (j + 1) + 16 * wave + n, last_row, g);
+        const VTile vn = load_vtile(v_bh, 64 * (j + 1) + 16 * wave, last_row, lane);
+        float z[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            float corr = 1.f, p[4] = {0.f, 0.f, 0.f, 0.f};
-            if (live[t]) {
-                const float mb = row16_max(fmaxf(fmaxf(z[t][0], z[t][1]), fmaxf(z[t][2], z[t][3])));
-                const float mn = fmaxf(m_run[t], mb);
-                corr = __expf(m_run[t] - mn);
-                float ls = 0.f;
+            v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int T4 = 0; T4 < 4; ++T4) {
-                    p[T4] = z[t][T4] == -INFINITY ? 0.f : __expf(z[t][T4] - mn);
-                    ls += p[T4];
-                }
-                l_part[t] = fmaf(l_part[t], corr, ls);
-                m_run[t] = mn;
-            }
-#pragma unroll
-            for (int T4 = 0; T4 < 4; ++T4) wp.p[16 * T4 + n][4 * t + g] = p[T4];
-            if (n == 0) wp.corr[4 * t + g] = corr;
+            for (int ks = 0; ks < 4; ++ks)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Aq[t][ks], __builtin_bit_cast(v8bf, kc.k[ks]),
+                                                              acc, 0, 0, 0);
+            z[t] = tok < L ? acc.x * a.scale : -INFINITY;
         }
+        softmax_tile<NT>(z, live, m_run, l_part, tp, g, n);
         wave_lds_fence();
-        pv_update<NT>(pv, wp, v_bh + (size_t)j * kBlock * kD, g, n, L - 64 * j);
+        pv_tile<NT>(pv, tp, vc);
         wave_lds_fence();
+        kc = kn;
+        vc = vn;
     }
 
     write_partials<NT>(sm.epi, pv, m_run, l_part, wave, lane, G, hq0, a.Hq, a.S, b, s, a.part_m,
@@ -109,32 +108,5 @@ __global__ __launch_bounds__(kThreads) void dense_decode_kernel(DenseArgs a) {
 
 template __global__ void dense_decode_kernel<1>(DenseArgs);
 template __global__ void dense_decode_kernel<2>(DenseArgs);
-
-// Log-sum-exp merge of the split partials (flash-decoding reduction): one workgroup per (b, h),
-// one thread per output dim.
-__global__ __launch_bounds__(kD) void lse_merge_kernel(const float* part_m, const float* part_l,
-                                                       const float* part_acc, int S, uint16_t* out,
-                                                       float* lse) {
-    const size_t bh = blockIdx.x;
-    const int d = threadIdx.x;
-    const float* pm = part_m + bh * S;
-    const float* pl = part_l + bh * S;
-    const float* pa = part_acc + bh * (size_t)S * kD + d;
-    float mx = -INFINITY;
-    for (int s = 0; s < S; ++s) mx = fmaxf(mx, pm[s]);
-    float l = 0.f, o = 0.f;
-    if (mx != -INFINITY) {
-        for (int s = 0; s < S; ++s) {
-            const float ms = pm[s];
-            if (ms != -INFINITY) {
-                const float w = __expf(ms - mx);
-                l = fmaf(w, pl[s], l);
-                o = fmaf(w, pa[(size_t)s * kD], o);
-            }
-        }
-    }
-    out[bh * kD + d] = f32_to_bf16(mx != -INFINITY ? o / l : 0.f);
-    if (lse && d == 0) lse[bh] = mx != -INFINITY ? mx + logf(l) : -INFINITY;
-}
 
 }  // namespace ffd

@@ -27,19 +27,29 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     return (uint16_t)(u >> 16);
 }
 
-// Reductions over the 16 lanes of one MFMA row group (lanes 16g..16g+15).
+// Reductions over the 16 lanes of one MFMA row group (lanes 16g..16g+15), every lane receiving
+// the result: DPP quad permutes (xor 1, xor 2) then row rotations by 4 and 8.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1;     // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;     // quad_perm [2,3,0,1]
+constexpr int kDppRor4 = 0x124;    // row_ror:4
+constexpr int kDppRor8 = 0x128;    // row_ror:8
+
 __device__ __forceinline__ float row16_max(float x) {
-    x = fmaxf(x, __shfl_xor(x, 1));
-    x = fmaxf(x, __shfl_xor(x, 2));
-    x = fmaxf(x, __shfl_xor(x, 4));
-    x = fmaxf(x, __shfl_xor(x, 8));
+    x = fmaxf(x, dpp_f<kDppXor1>(x));
+    x = fmaxf(x, dpp_f<kDppXor2>(x));
+    x = fmaxf(x, dpp_f<kDppRor4>(x));
+    x = fmaxf(x, dpp_f<kDppRor8>(x));
     return x;
 }
 __device__ __forceinline__ float row16_sum(float x) {
-    x += __shfl_xor(x, 1);
-    x += __shfl_xor(x, 2);
-    x += __shfl_xor(x, 4);
-    x += __shfl_xor(x, 8);
+    x += dpp_f<kDppXor1>(x);
+    x += dpp_f<kDppXor2>(x);
+    x += dpp_f<kDppRor4>(x);
+    x += dpp_f<kDppRor8>(x);
     return x;
 }
 __device__ __forceinline__ float wave_max(float x) {
@@ -59,66 +69,102 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Online-softmax state for the PV product of one wave, G_T = 4 * NT heads.
-// Lane (g, n) = (lane >> 4, lane & 15) accumulates tokens t = g (mod 4) of every block, dims
-// 8n..8n+7, for all heads. acc[h][e] is the unnormalised sum of p * v.
+// Work decomposition shared by both attention kernels: a workgroup of 4 waves serves one
+// (sequence, KV head, split); wave w owns tokens [16w, 16w + 16) of every 64-token block of the
+// split (one MFMA tile), so each wave keeps its own online-softmax state over its tiles and the
+// four states are merged in the epilogue.
+
+// PV accumulators of one wave for 4 * NT heads: lane l holds dims 2l and 2l + 1 of every head;
+// acc[h][e] is the unnormalised sum of p * v.
 template <int NT>
 struct PvAcc {
-    float acc[4 * NT][8];
+    float acc[4 * NT][2];
     __device__ __forceinline__ void zero() {
 #pragma unroll
-        for (int h = 0; h < 4 * NT; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+        for (int h = 0; h < 4 * NT; ++h) acc[h][0] = acc[h][1] = 0.f;
     }
 };
 
-// Per-wave LDS scratch for one block: probabilities p[token][head] and per-head rescale factors.
+// Per-wave LDS scratch for one tile: probabilities p[token][head] and per-head rescale factors.
 template <int NT>
-struct WaveP {
-    float p[kBlock][4 * NT];
+struct __attribute__((aligned(16))) TileP {
+    float p[16][4 * NT];
     float corr[4 * NT];
 };
 
-// acc[h] = acc[h] * corr[h] + sum over this lane's tokens of p[t][h] * V[t][8n..8n+7].
-// vblk points at V row 0 of the block (bf16 [64][128]); tokens at or after `valid` have p = 0 and
-// are skipped.
+// This lane's dword (dims 2l, 2l + 1) of the 16 value rows of a tile.
+struct VTile {
+    uint32_t v[16];
+};
+
+// Rows row0 .. row0 + 15 of v_bh (bf16 [rows][128]), each clamped to last_row: rows past the end
+// of the sequence read the last valid row, a finite value whose probability is zero, so no select
+// is needed and the loads stay unconditional (the compiler can count them).
+__device__ __forceinline__ VTile load_vtile(const uint16_t* v_bh, int row0, int last_row, int lane) {
+    const uint32_t* vp = reinterpret_cast<const uint32_t*>(v_bh) + lane;
+    VTile r;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) r.v[t] = vp[(size_t)min(row0 + t, last_row) * 64];
+    return r;
+}
+
+// acc[h] = acc[h] * corr[h] + sum_t p[t][h] * v[t]. Tokens go in groups of four with a scheduling
+// barrier between groups, so the compiler does not hoist all sixteen probability reads at once
+// (which would cost ~64 registers).
 template <int NT>
-__device__ __forceinline__ void pv_update(PvAcc<NT>& pv, const WaveP<NT>& wp, const uint16_t* vblk,
-                                          int g, int n, int valid) {
+__device__ __forceinline__ void pv_tile(PvAcc<NT>& pv, const TileP<NT>& tp, const VTile& vt) {
 #pragma unroll
     for (int h = 0; h < 4 * NT; ++h) {
-        const float c = wp.corr[h];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pv.acc[h][e] *= c;
-    }
-    const uint4* vp = reinterpret_cast<const uint4*>(vblk) + n;   // 16 uint4 per 128-dim row
-    uint4 vv[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int t = 4 * i + g;
-        vv[i] = t < valid ? vp[t * 16] : make_uint4(0, 0, 0, 0);
+        const float c = tp.corr[h];
+        pv.acc[h][0] *= c;
+        pv.acc[h][1] *= c;
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int t = 4 * i + g;
-        float v[8];
-        v[0] = bf16_lo(vv[i].x); v[1] = bf16_hi(vv[i].x);
-        v[2] = bf16_lo(vv[i].y); v[3] = bf16_hi(vv[i].y);
-        v[4] = bf16_lo(vv[i].z); v[5] = bf16_hi(vv[i].z);
-        v[6] = bf16_lo(vv[i].w); v[7] = bf16_hi(vv[i].w);
+    for (int t0 = 0; t0 < 16; t0 += 4) {
 #pragma unroll
-        for (int h = 0; h < 4 * NT; ++h) {
-            const float p = wp.p[t][h];
+        for (int t = t0; t < t0 + 4; ++t) {
+            const float v0 = bf16_lo(vt.v[t]), v1 = bf16_hi(vt.v[t]);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pv.acc[h][e] = fmaf(p, v[e], pv.acc[h][e]);
+            for (int q4 = 0; q4 < NT; ++q4) {
+                const float4 p = *reinterpret_cast<const float4*>(&tp.p[t][4 * q4]);
+                pv.acc[4 * q4 + 0][0] = fmaf(p.x, v0, pv.acc[4 * q4 + 0][0]);
+                pv.acc[4 * q4 + 0][1] = fmaf(p.x, v1, pv.acc[4 * q4 + 0][1]);
+                pv.acc[4 * q4 + 1][0] = fmaf(p.y, v0, pv.acc[4 * q4 + 1][0]);
+                pv.acc[4 * q4 + 1][1] = fmaf(p.y, v1, pv.acc[4 * q4 + 1][1]);
+                pv.acc[4 * q4 + 2][0] = fmaf(p.z, v0, pv.acc[4 * q4 + 2][0]);
+                pv.acc[4 * q4 + 2][1] = fmaf(p.z, v1, pv.acc[4 * q4 + 2][1]);
+                pv.acc[4 * q4 + 3][0] = fmaf(p.w, v0, pv.acc[4 * q4 + 3][0]);
+                pv.acc[4 * q4 + 3][1] = fmaf(p.w, v1, pv.acc[4 * q4 + 3][1]);
+            }
         }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Online-softmax update of one tile for the heads of this lane (head 4t + g, token n): keeps the
+// running max m_run and per-lane partial sum l_part, and writes p and the rescale factor to LDS.
+// Heads with use[t] false contribute p = 0 and keep their state.
+template <int NT>
+__device__ __forceinline__ void softmax_tile(const float (&z)[NT], const bool (&use)[NT], float (&m_run)[NT],
+                                             float (&l_part)[NT], TileP<NT>& tp, int g, int n) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        float corr = 1.f, p = 0.f;
+        if (use[t]) {
+            const float mn = fmaxf(m_run[t], row16_max(z[t]));
+            if (mn != -INFINITY) {                   // a tile wholly past the end changes nothing
+                corr = __expf(m_run[t] - mn);
+                p = z[t] == -INFINITY ? 0.f : __expf(z[t] - mn);
+                l_part[t] = fmaf(l_part[t], corr, p);
+                m_run[t] = mn;
+            }
+        }
+        tp.p[n][4 * t + g] = p;
+        if (n == 0) tp.corr[4 * t + g] = corr;
     }
 }
 
 // Workgroup epilogue: combine the four waves' (m, l, acc) and write this split's partial state.
-// m_w[h], l_w[h] are row-uniform per head (lane n == 0 of row g holds head 4t + g); pv holds
-// per-lane partial sums over tokens t = g (mod 4).
 template <int NT>
 struct EpilogueLds {
     float m[kWaves][4 * NT];
@@ -127,7 +173,7 @@ struct EpilogueLds {
 };
 
 template <int NT>
-__device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, PvAcc<NT>& pv,
+__device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<NT>& pv,
                                                const float (&m_run)[NT], const float (&l_part)[NT],
                                                int wave, int lane, int G, int hq0, int Hq, int S,
                                                int b, int s, float* part_m, float* part_l,
@@ -143,19 +189,7 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, PvAcc<NT>& pv
     }
 #pragma unroll
     for (int h = 0; h < 4 * NT; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float x = pv.acc[h][e];
-            x += __shfl_xor(x, 16);
-            x += __shfl_xor(x, 32);
-            pv.acc[h][e] = x;
-        }
-    if (g == 0) {
-#pragma unroll
-        for (int h = 0; h < 4 * NT; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) E.acc[wave][h][8 * n + e] = pv.acc[h][e];
-    }
+        *reinterpret_cast<float2*>(&E.acc[wave][h][2 * lane]) = make_float2(pv.acc[h][0], pv.acc[h][1]);
     __syncthreads();
     for (int idx = threadIdx.x; idx < G * kD; idx += kThreads) {
         const int h = idx >> 7, d = idx & (kD - 1);

@@ -8,8 +8,8 @@ namespace ffd {
 
 struct DecodeArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
-    const uint32_t* codes;      // [B, Hkv, Lcap/32, 64, 4]
-    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
+    const uint32_t* codes;      // [B, Hkv, Lcap/16, 64, 2]
+    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap]
     const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]
     const uint16_t* v;          // bf16 [B, Hkv, Lcap, 128]
     const int32_t* seq_lens;    // [B]
@@ -44,8 +44,8 @@ struct QuantArgs {
 
 template <int NT> __global__ void ffd_decode_kernel(DecodeArgs a);
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
-__global__ void lse_merge_kernel(const float* part_m, const float* part_l, const float* part_acc,
-                                 int S, uint16_t* out, float* lse);
 __global__ void quantize_keys_kernel(QuantArgs a);
+__global__ void lse_merge_kernel(const float* part_m, const float* part_l, const float* part_acc, int S,
+                                 uint16_t* out, float* lse);
 
 }  // namespace ffd

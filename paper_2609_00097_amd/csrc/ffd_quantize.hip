@@ -59,11 +59,11 @@ __global__ __launch_bounds__(kThreads) void quantize_keys_kernel(QuantArgs a) {
     word |= __shfl_xor(word, 1);                        // the pair of lanes covering 16 dims
     if (!live) return;
 
-    const int S = t >> 5, tt = (t >> 4) & 1, n16 = t & 15;
+    const int n16 = t & 15;
     if ((j16 & 1) == 0) {
         const int w = j16 >> 1;                         // 16-dim group 0..7
         const int cc = w >> 2, g = w & 3;
-        a.codes[((bh * (size_t)(a.Lcap / 32) + S) * 64 + n16 + 16 * g) * 4 + 2 * tt + cc] = word;
+        a.codes[((bh * (size_t)(a.Lcap / 64) + (t >> 6)) * 64 + n16 + 16 * g) * 8 + 2 * ((t >> 4) & 3) + cc] = word;
     }
     {
         const int cc = j16 >> 3, g = (j16 & 7) >> 1, e0 = 8 * (j16 & 1);

@@ -100,10 +100,15 @@ def workspace_bytes(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0) -
     return lib().ffd_workspace_bytes(B, Hq, Hkv, Lcap, HEAD_DIM, num_splits)
 
 
+def new_workspace(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0, device="cuda"):
+    """A workspace for either attention entry point (one per stream)."""
+    return torch.empty(max(workspace_bytes(B, Hq, Hkv, Lcap, num_splits), 16), dtype=torch.uint8,
+                       device=device)
+
+
 def quantized_shapes(B: int, Hkv: int, Lcap: int):
     """Shapes of (codes int32, absmax bf16, resid int8) for a cache of capacity Lcap."""
-    return ((B, Hkv, Lcap // 32, 64, 4), (B, Hkv, Lcap // 64, 16, 4),
-            (B, Hkv, Lcap // 16, 2, 64, 16))
+    return ((B, Hkv, Lcap // 64, 64, 8), (B, Hkv, Lcap // 64, 16, 4), (B, Hkv, Lcap // 16, 2, 64, 16))
 
 
 def empty_quantized(B: int, Hkv: int, Lcap: int, device):
@@ -154,9 +159,8 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
         _need(t, nm, dt, sh)
     out, lse, mask = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None,
                                    return_mask or mask is not None, out, lse, mask)
-    nbytes = workspace_bytes(B, Hq, Hkv, Lcap, num_splits)
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device)
     _check("ffd_decode_attention", lib().ffd_decode_attention(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
         D, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
@@ -175,9 +179,8 @@ def dense_decode_attention(q, k, v, seq_lens, *, num_splits: int = 0, softmax_sc
     _need(v, "v", torch.bfloat16, (B, Hkv, Lcap, D))
     _need(seq_lens, "seq_lens", torch.int32, (B,))
     out, lse, _ = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None, False, out, lse, None)
-    nbytes = workspace_bytes(B, Hq, Hkv, Lcap, num_splits)
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device)
     _check("ffd_dense_decode_attention", lib().ffd_dense_decode_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap, D, num_splits,
         float(softmax_scale), _ptr(out), _ptr(lse), _ptr(workspace),

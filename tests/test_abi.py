@@ -1,0 +1,82 @@
+"""The C-ABI library loads without a GPU, exports every symbol ffd.h declares, and rejects bad
+arguments with status codes before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ffd.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(ffd_\w+)\s*\(", src, re.M)))
+
+
+@pytest.fixture(scope="module")
+def so():
+    from paper_2609_00097_amd import ffd
+    if not os.path.exists(ffd.LIB_PATH):
+        pytest.skip("libffd.so not built (run __graft_entry__.build())")
+    return ffd.lib()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
+              "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_status_string"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(so):
+    for n in declared_functions():
+        assert hasattr(so, n), n
+
+
+def test_status_strings(so):
+    assert so.ffd_status_string(0) == b"FFD_OK"
+    assert so.ffd_status_string(3) == b"FFD_ERR_WORKSPACE_TOO_SMALL"
+    assert so.ffd_status_string(99) == b"FFD_ERR_UNKNOWN"
+
+
+def test_splits_and_workspace_sizes(so):
+    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 64
+    assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8
+    assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
+    assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
+    assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 64 * 130 * 4
+    assert so.ffd_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
+
+
+def _decode(so, **kw):
+    a = dict(q=None, codes=None, absmax=None, resid=None, v=None, lens=None, B=1, Hq=32, Hkv=8,
+             Lcap=4096, D=128, block=64, delta=5.0, n_sink=64, n_local=256, splits=0, scale=0.0,
+             out=None, lse=None, mask=None, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return so.ffd_decode_attention(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), 1),                                 # null pointers
+    (dict(D=96), 2), (dict(block=32), 2), (dict(Hq=12, Hkv=1), 2), (dict(Hq=30), 1),
+    (dict(Lcap=100), 1), (dict(delta=-1.0), 1), (dict(delta=float("nan")), 1),
+    (dict(n_sink=-1), 1), (dict(splits=2000), 1), (dict(B=0), 0),
+])
+def test_argument_checks_return_before_any_launch(so, kw, status):
+    assert _decode(so, **kw) == status
+
+
+def test_misaligned_and_small_workspace(so):
+    fake = 0x1000
+    args = dict(q=fake, codes=fake, absmax=fake, resid=fake, v=fake, lens=fake, out=fake, ws=fake)
+    assert _decode(so, **args, ws_bytes=16) == 3
+    assert _decode(so, **{**args, "q": fake + 2}, ws_bytes=1 << 30) == 1
+
+
+def test_quantize_range_checks(so):
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 10, 5, None) == 1
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 0, 5000, None) == 1
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 7, 7, None) == 0
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 96, 0, 1, None) == 2

@@ -111,6 +111,25 @@ def test_split_count_invariance():
     compare_ffd(c, 5.0, ref_out, ref_lse, ref_mask)
 
 
+def test_one_workspace_serves_repeated_and_alternating_calls():
+    """One workspace reused by repeated, alternating calls gives identical results."""
+    from paper_2609_00097_amd import ffd
+    c = I.small_case(seed=61, B=2, Hq=8, Hkv=2, seq_lens=(3000, 1200), heavy_frac=0.05)
+    up = Uploaded(c)
+    qk = _quant(up)
+    ws = ffd.new_workspace(c.B, c.Hq, c.Hkv, c.Lcap, 5, "cuda")
+    ref_out, ref_lse, ref_mask = _ffd(up, qk, 5.0, num_splits=5)
+    dref_out, dref_lse = ffd.dense_decode_attention(up.q, up.k, up.v, up.seq_lens, num_splits=5)
+    for _ in range(4):
+        out, lse, _ = ffd.decode_attention(up.q, *qk, up.v, up.seq_lens, delta=5.0, num_splits=5,
+                                           workspace=ws)
+        dout, dlse = ffd.dense_decode_attention(up.q, up.k, up.v, up.seq_lens, num_splits=5,
+                                                workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out) and torch.equal(lse, ref_lse)
+        assert torch.equal(dout, dref_out) and torch.equal(dlse, dref_lse)
+
+
 def test_argument_errors_return_status_without_launch():
     from paper_2609_00097_amd import ffd
     c = I.small_case(seed=1, B=1, Hq=8, Hkv=2, seq_lens=(100,))

@@ -5,22 +5,22 @@ from oracle import ffd_oracle as O
 
 
 def test_pack_codes_single_token_hand_checked():
-    """Token 17 of slab 0 (tt = 1, n = 1); dims 16..31 (cc = 0, g = 1) set to code 3 at dim 16+e
-    for e = 5 only -> lane 1 + 16 = 17, word 2*1 + 0 = 2, bit 8*(5%4) + 2*(5//4) = 10."""
-    codes = np.zeros((32, 128), dtype=np.int64)
-    codes[17, 16 + 5] = 3
+    """Token 81 is block 1, t4 = 1, n = 1; dim 16 + 5 is cc = 0, g = 1, e = 5 -> lane 1 + 16 = 17,
+    word 2*1 + 0 = 2, bit 8*(5%4) + 2*(5//4) = 10."""
+    codes = np.zeros((128, 128), dtype=np.int64)
+    codes[81, 16 + 5] = 3
     p = O.pack_codes(codes)
     nz = np.argwhere(p)
-    assert nz.tolist() == [[0, 17, 2]]
-    assert int(p[0, 17, 2]) == 3 << 10
+    assert nz.tolist() == [[1, 17, 2]]
+    assert int(p[1, 17, 2]) == 3 << 10
 
 
 def test_pack_codes_fast_equals_loop_and_roundtrips():
     rng = np.random.default_rng(0)
-    codes = rng.integers(0, 4, size=(96, 128))
+    codes = rng.integers(0, 4, size=(128, 128))
     p = O.pack_codes(codes)
     assert np.array_equal(O.pack_codes_fast(codes), p)
-    assert np.array_equal(O.unpack_codes(p, 96), codes)
+    assert np.array_equal(O.unpack_codes(p, 128), codes)
 
 
 def test_pack_absmax_and_resid_index_maps():
