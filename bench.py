@@ -80,24 +80,34 @@ def dense_bytes(case, S):
         2 * case.B * case.Hq * S * (case.D + 2) * 4
 
 
-def time_steps(fn, steps, warmup, flush, stream):
+def time_steps(fn, steps, warmup, flush, stream, stages=False):
+    """Event-timed steps, each after a cache flush. With ``stages``, ``fn(events)`` also records
+    four per-stage events inside the step (on the same stream); returns their [steps, 3] durations."""
     import torch
     for _ in range(warmup):
         flush.zero_()
-        fn()
+        fn() if not stages else fn(None)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    stage_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    if stages:
+        for evs in stage_evs:
+            for e in evs:
+                e.record(stream)            # create the events before the library records them
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
         flush.zero_()
         starts[i].record(stream)
-        fn()
+        fn() if not stages else fn(stage_evs[i])
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    return ms, wall
+    if not stages:
+        return ms, wall
+    st = np.array([[evs[k].elapsed_time(evs[k + 1]) for k in range(3)] for evs in stage_evs])
+    return ms, wall, st
 
 
 def cpu_baseline(case, delta, budget_s):
@@ -178,10 +188,10 @@ def main():
     lse = torch.empty((case.B, case.Hq), dtype=torch.float32, device=dev)
     mask = torch.empty((case.B, case.Hq, case.Lcap // 64), dtype=torch.uint8, device=dev)
 
-    def ffd_step(delta=args.delta):
+    def ffd_step(delta=args.delta, events=None):
         ffd.decode_attention(q, codes, absmax, resid, v, lens, delta=delta, n_sink=case.n_sink,
                              n_local=case.n_local, num_splits=args.splits, workspace=ws, out=out,
-                             lse=lse)
+                             lse=lse, stage_events=events)
 
     # the measured mask gives the algorithmic bytes (mask output off in the timed steps)
     def mask_for(delta):
@@ -195,6 +205,10 @@ def main():
     nbytes = algorithmic_bytes(case, keep, S)
 
     ms, wall = time_steps(ffd_step, args.steps, args.warmup, flush, stream)
+    # per-kernel durations from library-recorded events, in separate steps: the event markers
+    # between kernels add a few microseconds of gap, so these steps are not the headline figure
+    _, _, stage_ms = time_steps(lambda ev: ffd_step(events=ev), max(10, args.steps // 2), 3, flush,
+                                stream, stages=True)
     if args.profile_only:
         print(json.dumps({"profile_only": True, "ffd_us_mean": float(ms.mean() * 1e3)}))
         return
@@ -202,7 +216,7 @@ def main():
     tbps = nbytes["total"] / (us * 1e-6) / 1e12
 
     # dense flash-decode baseline, same protocol
-    dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev)
+    dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev, dense=True)
 
     def dense_step():
         ffd.dense_decode_attention(q, k, v, lens, num_splits=args.splits, workspace=dws, out=out,
@@ -220,6 +234,16 @@ def main():
         sweep[str(d)] = {"us": round(su, 2), "tbps": round(bd["total"] / (su * 1e-6) / 1e12, 3),
                          "keep_head_blocks": round(float(kd.mean()), 5),
                          "speedup_vs_dense": round(dense_us / su, 2)}
+
+    # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
+    stage_us = stage_ms.mean(axis=0) * 1e3
+    stage_bytes = {"ffd_scan_kernel": nbytes["scan"] + case.B * case.Hq * 2 * case.D,
+                   "ffd_refine_kernel": nbytes["gather"],
+                   "lse_merge_kernel": nbytes["partials"] // 2 + case.B * case.Hq * (2 * case.D + 4)}
+    names = list(stage_bytes)
+    dom = names[int(np.argmax(stage_us))]
+    dom_us = float(stage_us[names.index(dom)])
+    dom_gbps = stage_bytes[dom] / (dom_us * 1e-6) / 1e9
 
     G = case.G
     valid_blocks = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel()
@@ -255,11 +279,15 @@ def main():
         "delta_sweep": sweep,
         "quantize_cache_us": round(quant_ms * 1e3, 1),
         "wall_s_timed_region": round(wall, 3),
-        "roofline": {"bound": "hbm", "achieved": round(nbytes["total"] / (us * 1e-6) / 1e9, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(nbytes["total"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-                     "traffic": None,
-                     "kernel": "ffd_decode_kernel (one launch per step, split merge fused), HIP events"},
+        "stages_us": {k: round(float(u), 2) for k, u in zip(names, stage_us)},
+        "stages_gbps": {k: round(stage_bytes[k] / (float(u) * 1e-6) / 1e9, 1)
+                        for k, u in zip(names, stage_us)},
+        "roofline": {"bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": dom, "kernel_us": round(dom_us, 2),
+                     "algorithmic_bytes": int(stage_bytes[dom]),
+                     "timing": "HIP events recorded by the library on the launch stream around "
+                               "each kernel, mean over the timed steps"},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(case, args.delta, args.cpu_seconds)

@@ -8,8 +8,9 @@
  *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), 2-bit scan and
  *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement that reuses
  *                               the scan dot products (Eq. 4), online-softmax attention over the kept
- *                               blocks, split along the sequence and merged by log-sum-exp
- *                               (flash-decoding, Sec. 2 and Sec. 3.3).
+ *                               blocks, split into partial states merged by log-sum-exp
+ *                               (flash-decoding, Sec. 2 and Sec. 3.3). Three kernels in order on
+ *                               `stream`: scan + selection, refinement + attention, merge.
  *   ffd_dense_decode_attention  exact dense decode attention over the bf16 cache (the dense
  *                               comparator of Sec. 4.2), same split-and-merge scheme.
  *
@@ -88,15 +89,23 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
  *                m~_h is the max thumbnail score over tokens [0, n_sink) U [L - n_local, L).
  *                All scores carry softmax_scale. With n_sink = n_local = 0, m~ = -inf and every
  *                block is kept.
- *   num_splits   splits of each sequence's blocks (1..FFD_MAX_SPLITS), or 0 for automatic.
+ *   num_splits   refinement workgroups per KV group on average (1..FFD_MAX_SPLITS), or 0 for
+ *                automatic: the call uses W = num_splits * B * Hkv refinement workgroups in all,
+ *                given to the KV groups in proportion to their kept blocks (at least one each),
+ *                each refining an equal run of its group's kept blocks in block order; their
+ *                partial states are merged by log-sum-exp.
  *   softmax_scale  > 0, or 0 for 1/sqrt(D).
  *   out          bf16  [B, Hq, D]  softmax(z over kept tokens) . V, z the refined logits;
  *                                   0 for a head with no kept token (empty sequence).
  *   lse          float [B, Hq] or NULL: ln sum exp(z) over kept tokens (-inf if none).
  *   block_mask   uint8 [B, Hq, Lcap/64] or NULL: 1 iff head h kept block j; 0 at/after the end.
  *   workspace    device scratch of at least ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)
- *                bytes holding the split partials; it needs no initialisation and is clobbered.
- *                Calls that overlap in time (different streams) need separate workspaces.
+ *                bytes: the partials, a per-KV-group table locating them, the scan's kept-block
+ *                lists and counts, and the scan scores of kept blocks (written by the scan kernel,
+ *                read by the refinement kernel; 1 KiB per block for G <= 4, 2 KiB for G = 8,
+ *                reserved for every block of the capacity). It needs no initialisation and is
+ *                clobbered. Calls that overlap in time (different streams) need separate workspaces.
+ *  Limits: B * Hkv <= 2^20 and Lcap <= 2^24 tokens, else FFD_ERR_UNSUPPORTED.
  */
 int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax,
                          const void* k_resid, const void* v, const int32_t* seq_lens,
@@ -106,9 +115,24 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * ffd_decode_attention with stage timing, for measurement: when stage_events is not NULL it must
+ * point to four events created by the caller (hipEventCreate); they are recorded on `stream` before
+ * the scan kernel, between scan and refinement, between refinement and merge, and after the merge.
+ * Everything else is as for ffd_decode_attention (which is this call with stage_events = NULL).
+ */
+int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
+                                const void* k_resid, const void* v, const int32_t* seq_lens,
+                                int B, int Hq, int Hkv, int Lcap, int D, int block_size, float delta,
+                                int n_sink, int n_local, int num_splits, float softmax_scale,
+                                void* out, float* lse, uint8_t* block_mask,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                hipEvent_t* stage_events);
+
+/*
  * Exact dense decode attention over bf16 keys and values (the FlashAttention-2 comparator of
  * Sec. 4.2): out = softmax(softmax_scale * q K^T) V over tokens [0, seq_lens[b]).
- * Arguments as above; k is bf16 [B, Hkv, Lcap, D].
+ * Arguments as above; k is bf16 [B, Hkv, Lcap, D]; num_splits splits each sequence's blocks into
+ * equal runs; the workspace needs ffd_dense_workspace_bytes(...) bytes.
  */
 int ffd_dense_decode_attention(const void* q, const void* k, const void* v, const int32_t* seq_lens,
                                int B, int Hq, int Hkv, int Lcap, int D, int num_splits,
@@ -118,10 +142,17 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
 /* Number of splits a call with this num_splits (0 = automatic) will use. 0 on invalid input. */
 int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
-/* Workspace bytes needed by either attention entry point for these arguments:
- * B * Hq * S * (D + 2) * 4 (fp32 partials m, l, acc) with S = ffd_resolve_splits(...).
- * 0 on invalid input. */
+/* Workspace bytes needed by ffd_decode_attention for these arguments (enough for the dense entry
+ * point too). With S = ffd_resolve_splits(...), P = B * Hkv KV groups, G = Hq / Hkv, C = Lcap / 64
+ * blocks and S1 scan splits per group (chosen by the library from B, Hkv, Lcap), the regions, each
+ * starting on a 256-byte boundary, are: partials (S * P + P) * G * (D + 2) * 4 bytes, table P * 8,
+ * kept counts P * S1 * 4, kept lists P * C * 4, scan scores P * C * 1024 * (G <= 4 ? 1 : 2).
+ * 0 on invalid or unsupported input. */
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
+
+/* Workspace bytes needed by ffd_dense_decode_attention: B * Hq * S * (D + 2) * 4 (fp32 partials
+ * m, l, acc) with S = ffd_resolve_splits(...). 0 on invalid input. */
+size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
 
 /* Static, human-readable name of a status code. */
 const char* ffd_status_string(int status);

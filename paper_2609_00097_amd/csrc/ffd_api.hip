@@ -10,7 +10,7 @@ using namespace ffd;
 
 namespace {
 
-constexpr int kTargetWorkgroups = 2048;   // ~8 per CU on 256 CUs
+constexpr int kTargetWorkgroups = 512;    // two per CU on 256 CUs
 constexpr int kMinBlocksPerSplit = 8;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -44,12 +44,16 @@ int launch_status() {
     return e == hipSuccess ? FFD_OK : FFD_ERR_HIP;
 }
 
-// Workspace: split partials m [B,Hq,S], l [B,Hq,S], acc [B,Hq,S,D] (fp32).
+// Workspace: split partials m [B,Hq,S], l [B,Hq,S], acc [B,Hq,S,D] (fp32); the FFD path adds the
+// scan kernel's per-block keep bits and the scan scores of kept blocks.
 struct Partials {
     float* m;
     float* l;
     float* acc;
 };
+
+constexpr size_t kAlign = 256;
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 size_t partials_bytes(int B, int Hq, int S, int D) { return (size_t)B * Hq * S * (D + 2) * sizeof(float); }
 
@@ -57,6 +61,47 @@ Partials carve(void* ws, int B, int Hq, int S) {
     const size_t rows = (size_t)B * Hq * S;
     float* base = static_cast<float*>(ws);
     return Partials{base, base + rows, base + 2 * rows};
+}
+
+int head_tiles(int G) { return G <= 4 ? 1 : 2; }
+
+// Workgroups of the scan kernel per (sequence, KV head): about kScanWorkgroups in all, each scanning
+// at least kMinScanBlocks blocks so the pseudo-max and query setup stay a small part of its work, and
+// at most kFfdMaxScanBlocks (its kept list is staged in LDS).
+constexpr int kScanWorkgroups = 1024;
+constexpr int kMinScanBlocks = 16;
+
+int scan_splits(int B, int Hkv, int Lcap) {
+    const long long pairs = (long long)B * Hkv;
+    const long long nblk_cap = Lcap / FFD_BLOCK;
+    long long s = (kScanWorkgroups + pairs - 1) / pairs;
+    const long long cap = nblk_cap / kMinScanBlocks;
+    if (s > cap) s = cap;
+    const long long need = (nblk_cap + kFfdMaxScanBlocks - 1) / kFfdMaxScanBlocks;
+    if (s < need) s = need;
+    if (s < 1) s = 1;
+    return (int)s;
+}
+
+// FFD workspace: partials for W + B*Hkv refinement workgroups (W = S * B * Hkv) of G heads each,
+// the per-group (first workgroup, count) table, the scan's per-split kept counts and kept lists,
+// and the scan scores of kept blocks.
+struct FfdWorkspace {
+    size_t rows;                      // partial rows
+    size_t table_off, counts_off, lists_off, shat_off, total;
+};
+
+FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
+    FfdWorkspace w;
+    const size_t pairs = (size_t)B * Hkv;
+    const size_t nblk_cap = (size_t)(Lcap / FFD_BLOCK);
+    w.rows = ((size_t)S * pairs + pairs) * (size_t)(Hq / Hkv);
+    w.table_off = round_up(w.rows * (D + 2) * sizeof(float), kAlign);
+    w.counts_off = w.table_off + round_up(pairs * 2 * sizeof(int), kAlign);
+    w.lists_off = w.counts_off + round_up(pairs * scan_splits(B, Hkv, Lcap) * sizeof(int), kAlign);
+    w.shat_off = w.lists_off + round_up(pairs * nblk_cap * sizeof(uint32_t), kAlign);
+    w.total = w.shat_off + pairs * nblk_cap * 4 * head_tiles(Hq / Hkv) * 64 * sizeof(float);
+    return w;
 }
 
 int attention_common_checks(const void* q, const void* v, const int32_t* seq_lens, int B, int Hq,
@@ -74,7 +119,6 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
         return FFD_ERR_INVALID_ARGUMENT;
     const int S = resolve_splits(B, Hkv, Lcap, num_splits);
     if (S <= 0) return FFD_ERR_INVALID_ARGUMENT;
-    if (ws_bytes < ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)) return FFD_ERR_WORKSPACE_TOO_SMALL;
     *S_out = S;
     return FFD_OK;
 }
@@ -88,6 +132,14 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
 }
 
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
+    if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
+    const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
+    if (S <= 0) return 0;
+    if ((long long)B * Hkv > (1LL << 20) || Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return 0;
+    return ffd_layout(B, Hq, Hkv, Lcap, D, S).total;
+}
+
+size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
     const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
     if (S <= 0) return 0;
@@ -121,11 +173,12 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
     return launch_status();
 }
 
-int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax, const void* k_resid,
-                         const void* v, const int32_t* seq_lens, int B, int Hq, int Hkv, int Lcap, int D,
-                         int block_size, float delta, int n_sink, int n_local, int num_splits,
-                         float softmax_scale, void* out, float* lse, uint8_t* block_mask,
-                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
+                                const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
+                                int Hkv, int Lcap, int D, int block_size, float delta, int n_sink,
+                                int n_local, int num_splits, float softmax_scale, void* out, float* lse,
+                                uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream, hipEvent_t* stage_events) {
     if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
     if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
     int S = 0;
@@ -134,23 +187,59 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
     if (st != FFD_OK || B == 0) return st;
     if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
     if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
+    if ((long long)B * Hkv > (1LL << 20)) return FFD_ERR_UNSUPPORTED;
+    if (Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return FFD_ERR_UNSUPPORTED;
+    if (workspace_bytes < ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)) return FFD_ERR_WORKSPACE_TOO_SMALL;
     const int G = Hq / Hkv;
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
-    const Partials P = carve(workspace, B, Hq, S);
-    DecodeArgs a{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
-                 static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid),
-                 static_cast<const uint16_t*>(v), seq_lens, P.m, P.l, P.acc, block_mask, Hq, Hkv,
-                 Lcap, G, S, delta, scale, n_sink, n_local};
-    const dim3 grid((unsigned)S, (unsigned)Hkv, (unsigned)B);
+    const FfdWorkspace W = ffd_layout(B, Hq, Hkv, Lcap, D, S);
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    float* part_m = reinterpret_cast<float*>(ws);
+    float* part_l = part_m + W.rows;
+    float* part_acc = part_l + W.rows;
+    int2* table = reinterpret_cast<int2*>(ws + W.table_off);
+    int* counts = reinterpret_cast<int*>(ws + W.counts_off);
+    uint32_t* lists = reinterpret_cast<uint32_t*>(ws + W.lists_off);
+    float* shat = reinterpret_cast<float*>(ws + W.shat_off);
+    const int S1 = scan_splits(B, Hkv, Lcap);
+    const int npairs = B * Hkv;
+    const int Wr = S * npairs;
+    ScanArgs sa{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
+                static_cast<const uint16_t*>(k_absmax), seq_lens, lists, counts, shat, block_mask, Hq, Hkv,
+                Lcap, G, S1, delta, scale, n_sink, n_local};
+    RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_absmax),
+                  static_cast<const int8_t*>(k_resid), static_cast<const uint16_t*>(v), seq_lens, lists,
+                  counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale};
+    const dim3 scan_grid((unsigned)S1, (unsigned)Hkv, (unsigned)B);
+    const dim3 refine_grid((unsigned)(Wr + npairs));
+    auto mark = [&](int i) {
+        return stage_events && hipEventRecord(stage_events[i], stream) != hipSuccess ? FFD_ERR_HIP : FFD_OK;
+    };
+    if ((st = mark(0)) != FFD_OK) return st;
     if (G <= 4)
-        hipLaunchKernelGGL(ffd_decode_kernel<1>, grid, dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL(ffd_scan_kernel<1>, scan_grid, dim3(kThreads), 0, stream, sa);
     else
-        hipLaunchKernelGGL(ffd_decode_kernel<2>, grid, dim3(kThreads), 0, stream, a);
-    st = launch_status();
-    if (st != FFD_OK) return st;
-    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, P.m, P.l,
-                       P.acc, S, static_cast<uint16_t*>(out), lse);
-    return launch_status();
+        hipLaunchKernelGGL(ffd_scan_kernel<2>, scan_grid, dim3(kThreads), 0, stream, sa);
+    if ((st = launch_status()) != FFD_OK || (st = mark(1)) != FFD_OK) return st;
+    if (G <= 4)
+        hipLaunchKernelGGL(ffd_refine_kernel<1>, refine_grid, dim3(kThreads), 0, stream, ra);
+    else
+        hipLaunchKernelGGL(ffd_refine_kernel<2>, refine_grid, dim3(kThreads), 0, stream, ra);
+    if ((st = launch_status()) != FFD_OK || (st = mark(2)) != FFD_OK) return st;
+    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, part_m, part_l,
+                       part_acc, 0, table, G, static_cast<uint16_t*>(out), lse);
+    if ((st = launch_status()) != FFD_OK) return st;
+    return mark(3);
+}
+
+int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax, const void* k_resid,
+                         const void* v, const int32_t* seq_lens, int B, int Hq, int Hkv, int Lcap, int D,
+                         int block_size, float delta, int n_sink, int n_local, int num_splits,
+                         float softmax_scale, void* out, float* lse, uint8_t* block_mask,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return ffd_decode_attention_events(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
+                                       block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
+                                       lse, block_mask, workspace, workspace_bytes, stream, nullptr);
 }
 
 int ffd_dense_decode_attention(const void* q, const void* k, const void* v, const int32_t* seq_lens, int B,
@@ -162,6 +251,8 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
                                      lse, workspace, workspace_bytes, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k || !aligned16(k)) return FFD_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits))
+        return FFD_ERR_WORKSPACE_TOO_SMALL;
     const int G = Hq / Hkv;
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
     const Partials P = carve(workspace, B, Hq, S);
@@ -175,7 +266,7 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
     st = launch_status();
     if (st != FFD_OK) return st;
     hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, P.m, P.l,
-                       P.acc, S, static_cast<uint16_t*>(out), lse);
+                       P.acc, S, nullptr, 1, static_cast<uint16_t*>(out), lse);
     return launch_status();
 }
 

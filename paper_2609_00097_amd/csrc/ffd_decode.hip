@@ -1,31 +1,34 @@
-// FFD decode attention for gfx950: 2-bit scan + top-delta selection + refinement + online softmax.
+// FFD decode attention for gfx950: 2-bit scan + top-delta selection, then refinement + online
+// softmax over the kept blocks.
 //
 // Method (Alg. 1; Eq. 1-4): for each query head h of a KV group,
 //   s_hat[t] = alpha * q . k^quant_t                      (thumbnail scan)
 //   m~       = max of s_hat over the first n_sink and last n_local tokens      (pseudo-max, Eq. 3)
 //   keep j   iff max_{t in block j} s_hat[t] >= m~ - delta                       (top-delta, Eq. 1)
 //   z[t]     = s_hat[t] + alpha * q . k^res_t   for t in kept blocks            (scan reuse, Eq. 4)
-//   out      = softmax(z) . V over kept tokens, split along the sequence and merged by LSE.
+//   out      = softmax(z) . V over kept tokens, split into partial states merged by LSE.
 //
-// Mapping to the hardware. A workgroup (4 waves) serves one (sequence, KV head, split); wave w
-// owns the 16-token tile w of every 64-token block. The group's queries stay in registers as the A
-// operand of v_mfma_i32_16x16x64_i8: each query is held in fixed point Q = rint(q * 2^(22-E))
-// (|q| < 2^E), split into three signed 8-bit limbs, one MFMA row per (head, limb). The B operand is
-// either the tile's 2-bit codes expanded to bytes (two VALU ops per 4 codes) or the stored int8
-// residual, so both dot products are exact integer sums, combined and rounded once to fp32:
+// Arithmetic. The group's queries are the A operand of v_mfma_i32_16x16x64_i8: each query is held in
+// fixed point Q = rint(q * 2^(22-E)) (|q| < 2^E), split into three signed 8-bit limbs, one MFMA row
+// per (head, limb). The B operand is either a 16-token tile's 2-bit codes expanded to bytes (two VALU
+// ops per 4 codes) or its stored int8 residual, so both dot products are exact integer sums,
+// combined and rounded once to fp32:
 //   sum_d Q_d (2 c_d - 3) = T  (int32, exact),     s_hat = T * M_t * alpha 2^(E-23) / 1.5
 //   sum_d Q_d r_d         = R  (three int32 limbs), z = s_hat + R * M_t * alpha 2^(E-22) / 381
 // Output register i of lane (g, n) is row 4g + i, column n: head g's limbs for token n, so each
 // 16-lane row group owns one head and a tile's maximum is a 16-lane DPP reduction.
 //
-// Schedule. Wave w of a workgroup owns blocks w, w+4, w+8, ... of the split and keeps its own
-// online-softmax state; there is no barrier after the pseudo-max. Each wave streams its blocks'
-// codes and absmaxes through a ring of kRing register slots, refilling a slot as soon as it is
-// scored, so kRing blocks stay in flight. It takes the keep decision for each block itself and
-// parks a kept block's scan scores in its own small LDS queue; after each round of kRing blocks it
-// fetches each queued block's int8 residual and values tile by tile (two 16-token tiles in flight),
-// refines the parked scan scores (Eq. 4) and updates its softmax and PV state, while the ring's
-// scan loads keep streaming.
+// Two kernels, so that each stage's HBM stream is balanced over the whole chip:
+//  * ffd_scan_kernel streams the codes and absmaxes of every block once (the dominant, perfectly
+//    regular stream) and takes the keep decision per (head, block). For each kept block it stores
+//    the scan scores s_hat (the Eq. 4 reuse term) and appends the block, with its per-head keep bits,
+//    to its workgroup's kept list (in block order) in the workspace, plus the list's length.
+//  * ffd_refine_kernel gives each (sequence, KV head) a number of workgroups proportional to its
+//    kept blocks (every workgroup computes the same allocation from the scan's counts, so no
+//    cross-workgroup synchronisation is needed); each workgroup refines an equal share of its KV
+//    group's kept blocks, wave w taking 16-token tile w of every block, with several tiles' residual
+//    and value loads in flight, and writes one partial (m, l, acc) per head. lse_merge_kernel
+//    combines the partials of each head, located through a small per-group table.
 #include "ffd_device.h"
 #include "ffd_kernels.h"
 
@@ -33,8 +36,20 @@ namespace ffd {
 
 namespace {
 
-constexpr int kRing = 4;    // scan loads in flight per wave (blocks)
-constexpr int kPMW = 2;     // pseudo-max window blocks per wave per pass
+#ifndef FFD_SCAN_RING
+#define FFD_SCAN_RING 4
+#endif
+#ifndef FFD_REFINE_RING
+#define FFD_REFINE_RING 2
+#endif
+#ifndef FFD_REFINE_OCC
+#define FFD_REFINE_OCC 3
+#endif
+constexpr int kRing = FFD_SCAN_RING;          // scan loads in flight per wave (blocks)
+constexpr int kPMW = 2;                       // pseudo-max window blocks per wave per pass
+constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
+constexpr int kChunk = kFfdChunk;             // list entries staged per pass of the refinement kernel
+constexpr int kWaveList = kFfdMaxScanBlocks / kWaves;   // kept blocks one scan wave can hold
 
 __device__ __forceinline__ int limb_of(int Q, int which) {
     const int l0 = ((Q + 128) & 255) - 128;
@@ -62,138 +77,30 @@ struct HeadConsts {
     bool live[NT];     // head 4t + g exists
 };
 
-// One lane's share of a block's thumbnail: 32 B of codes (both 64-dim halves of its token in each
-// of the four tiles) and the absmax of its four tokens.
-struct BlockScan {
-    uint4 w0, w1;
-    uint2 mm;
-};
-
-__device__ __forceinline__ BlockScan load_block_scan(const uint32_t* __restrict__ codes_bh,
-                                                     const uint16_t* __restrict__ absmax_bh, int j,
-                                                     int lane) {
-    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + ((size_t)j * 64 + lane) * 2;
-    BlockScan r;
-    r.w0 = cp[0];
-    r.w1 = cp[1];
-    r.mm = *reinterpret_cast<const uint2*>(absmax_bh + (size_t)j * 64 + (lane & 15) * 4);
-    return r;
-}
-
-// Thumbnail scores of block j for this lane's head(s) and tokens 64j + 16*T4 + n.
 template <int NT>
-__device__ __forceinline__ void block_scores(const BlockScan& ld, int j, int lane, int L,
-                                             const HeadConsts<NT>& hc, float (&sc)[NT][4],
-                                             float (&M)[4]) {
-    const int n = lane & 15;
-    M[0] = bf16_lo(ld.mm.x); M[1] = bf16_hi(ld.mm.x);
-    M[2] = bf16_lo(ld.mm.y); M[3] = bf16_hi(ld.mm.y);
-    const uint32_t words[8] = {ld.w0.x, ld.w0.y, ld.w0.z, ld.w0.w, ld.w1.x, ld.w1.y, ld.w1.z, ld.w1.w};
-#pragma unroll
-    for (int T4 = 0; T4 < 4; ++T4) {
-        const v4i b0 = expand_codes(words[2 * T4 + 0]);
-        const v4i b1 = expand_codes(words[2 * T4 + 1]);
-        const bool valid = 64 * j + 16 * T4 + n < L;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            v4i acc = {0, 0, 0, 0};
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], b0, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], b1, acc, 0, 0, 0);
-            const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
-            const int T = (int)(2u * s - (uint32_t)hc.off[t]);     // exact modulo 2^32, |T| < 2^31
-            sc[t][T4] = valid ? (float)T * (M[T4] * hc.kap[t]) : -INFINITY;
-        }
-    }
-}
-
-// A kept block parked by one wave: its scan scores per (tile, head-tile, lane), absmaxes, index and
-// per-head keep bits (bit 4t + g).
-template <int NT>
-struct Parked {
-    float sc[4][NT][64];
-    float M[4][16];
-    int j;
-    uint32_t keep;
-};
-
-// One wave's fetch for one 16-token tile of a kept block: int8 residual and its lane's value dwords.
-struct TileGather {
-    v4i r0, r1;
-    VTile vt;
-};
-
-__device__ __forceinline__ TileGather load_tile_gather(const int8_t* __restrict__ resid_bh,
-                                                       const uint16_t* __restrict__ v_bh, int tile,
-                                                       int lane, int L) {
-    TileGather r;
-    const v4i* rp = reinterpret_cast<const v4i*>(resid_bh) + (size_t)tile * 128 + lane;
-    r.r0 = rp[0];
-    r.r1 = rp[64];
-    r.vt = load_vtile(v_bh, 16 * tile, max(L, 1) - 1, lane);
-    return r;
-}
-
-template <int NT>
-struct DecodeLds {
+struct QueryLds {
     alignas(16) int8_t limbs[4][4 * NT][kD];     // [limb][head][dim]; limb 3 is zero
     int off[4 * NT];
     float kap[4 * NT];
     float kap2[4 * NT];
-    float pm[kWaves][4 * NT];
-    Parked<NT> park[kWaves][kRing];
-    TileP<NT> tp[kWaves];
-    EpilogueLds<NT> epi;
 };
 
-}  // namespace
-
+// This lane's dword (dims 2*lane, 2*lane + 1) of the queries of heads wave + 4t of the group.
 template <int NT>
-__global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
-    __shared__ DecodeLds<NT> sm;
-    const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int g = lane >> 4, n = lane & 15;
-    const int G = a.G, hq0 = kvh * G;
-    const size_t bh = (size_t)b * a.Hkv + kvh;
-    const int L = min(max(a.seq_lens[b], 0), a.Lcap);
-    const int nblk = (L + kBlock - 1) / kBlock;
-    const int nblk_cap = a.Lcap / kBlock;
-    const int bps = (nblk + a.S - 1) / a.S;
-    const int jb = min(s * bps, nblk), je = min(jb + bps, nblk);
-
-    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * 8;
-    const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
-    const int8_t* resid_bh = a.resid + bh * (size_t)a.Lcap * kD;
-    const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
-
-    // Ring of this wave's scan loads: slot r holds block jb + 4*(i0 + r) + wave of round i0.
-    // The first chunk and the first pseudo-max window blocks are requested before the setup.
-    // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
-    // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
-    // draining every load in flight. Order: queries, pseudo-max window blocks, the first chunk.
-    uint32_t qw[NT];
+__device__ __forceinline__ void load_query_words(const uint16_t* __restrict__ q, int b, int Hq, int hq0,
+                                                 int G, int wave, int lane, uint32_t (&qw)[NT]) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-        qw[t] = reinterpret_cast<const uint32_t*>(a.q + ((size_t)b * a.Hq + hq0 + min(wave + 4 * t, G - 1)) * kD)[lane];
-    const int jlast = max(nblk, 1) - 1;
-    const int sink_end = min(a.n_sink, L);
-    const int loc_beg = max(0, L - a.n_local);
-    const int sink_blk_end = (sink_end + kBlock - 1) / kBlock;
-    const int loc_blk_beg = max(loc_beg / kBlock, sink_blk_end);
-    const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
-    auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
-    BlockScan win[kPMW];
-#pragma unroll
-    for (int i = 0; i < kPMW; ++i)
-        win[i] = load_block_scan(codes_bh, absmax_bh, min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
-    BlockScan ring[kRing];
-#pragma unroll
-    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan(codes_bh, absmax_bh, min(jb + kWaves * i + wave, jlast), lane);
+        qw[t] = reinterpret_cast<const uint32_t*>(q + ((size_t)b * Hq + hq0 + min(wave + 4 * t, G - 1)) * kD)[lane];
+}
 
-
-    // ---- queries -> fixed point limbs in LDS, per-head constants ------------------------------
-    // Head h (wave h % 4): E with max|q| < 2^E, Q = rint(q 2^(22-E)) split into three signed bytes
-    // stored as limbs[limb][h][d]; the fourth limb row and heads past G stay zero.
+// Queries -> fixed-point limbs in LDS and this lane's per-head constants. Head h (wave h % 4): E with
+// max|q| < 2^E, Q = rint(q 2^(22-E)) split into three signed bytes stored as limbs[limb][h][d]; the
+// fourth limb row and heads past G stay zero. Contains two workgroup barriers.
+template <int NT>
+__device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint32_t (&qw)[NT], int G,
+                                                   float scale, int tid, HeadConsts<NT>& hc) {
+    const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, n = lane & 15;
     for (int i = tid; i < 4 * 4 * NT * kD / 4; i += kThreads) reinterpret_cast<int*>(sm.limbs)[i] = 0;
     __syncthreads();
 #pragma unroll
@@ -214,13 +121,11 @@ __global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
         const int sum = wave_sum_i(Q0 + Q1);
         if (lane == 0) {
             sm.off[h] = 3 * sum;
-            sm.kap[h] = ldexpf(a.scale / 1.5f, E - 23);
-            sm.kap2[h] = ldexpf(a.scale / 381.f, E - 22);
+            sm.kap[h] = ldexpf(scale / 1.5f, E - 23);
+            sm.kap2[h] = ldexpf(scale / 381.f, E - 22);
         }
     }
     __syncthreads();
-
-    HeadConsts<NT> hc;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         // A operand: row m = n is (head 4t + n/4, limb n%4); its 16 bytes are dims 64cc + 16g + e.
@@ -234,6 +139,188 @@ __global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
         hc.kap[t] = hc.live[t] ? sm.kap[hh] : 0.f;
         hc.kap2[t] = hc.live[t] ? sm.kap2[hh] : 0.f;
     }
+}
+
+// One lane's share of a block's thumbnail: 32 B of codes (both 64-dim halves of its token in each
+// of the four tiles) and the absmax of its four tokens.
+struct BlockScan {
+    uint4 w0, w1;
+    uint2 mm;
+};
+
+__device__ __forceinline__ BlockScan load_block_scan(const uint32_t* __restrict__ codes_bh,
+                                                     const uint16_t* __restrict__ absmax_bh, int j,
+                                                     int lane) {
+    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + ((size_t)j * 64 + lane) * 2;
+    BlockScan r;
+    r.w0 = cp[0];
+    r.w1 = cp[1];
+    r.mm = *reinterpret_cast<const uint2*>(absmax_bh + (size_t)j * 64 + (lane & 15) * 4);
+    return r;
+}
+
+// Thumbnail scores of block j for this lane's head(s) and tokens 64j + 16*T4 + n; -inf past L.
+template <int NT>
+__device__ __forceinline__ void block_scores(const BlockScan& ld, int j, int lane, int L,
+                                             const HeadConsts<NT>& hc, float (&sc)[NT][4]) {
+    const int n = lane & 15;
+    const float M[4] = {bf16_lo(ld.mm.x), bf16_hi(ld.mm.x), bf16_lo(ld.mm.y), bf16_hi(ld.mm.y)};
+    const uint32_t words[8] = {ld.w0.x, ld.w0.y, ld.w0.z, ld.w0.w, ld.w1.x, ld.w1.y, ld.w1.z, ld.w1.w};
+#pragma unroll
+    for (int T4 = 0; T4 < 4; ++T4) {
+        const v4i b0 = expand_codes(words[2 * T4 + 0]);
+        const v4i b1 = expand_codes(words[2 * T4 + 1]);
+        const bool valid = 64 * j + 16 * T4 + n < L;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            v4i acc = {0, 0, 0, 0};
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], b0, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], b1, acc, 0, 0, 0);
+            const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
+            const int T = (int)(2u * s - (uint32_t)hc.off[t]);     // exact modulo 2^32, |T| < 2^31
+            sc[t][T4] = valid ? (float)T * (M[T4] * hc.kap[t]) : -INFINITY;
+        }
+    }
+}
+
+template <int NT>
+struct ScanLds {
+    QueryLds<NT> qs;
+    float pm[kWaves][4 * NT];
+    uint32_t kept[kWaves][kWaveList];    // each wave's kept blocks, in block order
+    int nkept[kWaves];
+};
+
+// ---- refinement helpers ---------------------------------------------------------------------
+
+// One wave's loads for one 16-token tile of a kept block: int8 residual, its lane's value dwords,
+// the stored scan scores of its heads and the token's absmax.
+template <int NT>
+struct RefineTile {
+    v4i r0, r1;
+    VTile vt;
+    float sc[NT];
+    uint32_t m;       // absmax bf16 bits in the low half
+};
+
+template <int NT>
+__device__ __forceinline__ RefineTile<NT> load_refine_tile(const int8_t* __restrict__ resid_bh,
+                                                           const uint16_t* __restrict__ v_bh,
+                                                           const float* __restrict__ shat_bh,
+                                                           const uint16_t* __restrict__ absmax_bh,
+                                                           int j, int T4, int lane, int last_row) {
+    RefineTile<NT> r;
+    const int tile = 4 * j + T4;
+    const v4i* rp = reinterpret_cast<const v4i*>(resid_bh) + (size_t)tile * 128 + lane;
+    r.r0 = rp[0];
+    r.r1 = rp[64];
+    r.vt = load_vtile(v_bh, 16 * tile, last_row, lane);
+    const float* sp = shat_bh + (size_t)tile * (NT * 64) + lane;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) r.sc[t] = sp[64 * t];
+    r.m = absmax_bh[(size_t)j * 64 + (lane & 15) * 4 + T4];
+    return r;
+}
+
+// Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum.
+__device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int incl = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int s = wsum[w];
+        before += w < wave ? s : 0;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + incl - x;
+}
+
+constexpr int kPairChunk = 4 * kThreads;     // KV groups allocated per pass (4 per thread)
+constexpr int kCountCache = 4096;            // scan counts kept in LDS when they all fit
+
+template <int NT>
+struct RefineLds {
+    QueryLds<NT> qs;
+    int wsum[kWaves];
+    int sel[4];                          // this workgroup's KV group: pair, first workgroup, workgroups, kept
+    int pn[kPairChunk];                  // kept blocks per KV group of the current pass
+    int cnt[kCountCache];                // all scan counts, when they fit
+    int pref[kFfdMaxScanSplits + 1];     // exclusive prefix of the group's per-scan-split kept counts
+    TileP<NT> tp[kWaves];
+    union {
+        uint32_t list[kChunk];           // kept blocks of the share: j | keep bits << 24
+        EpilogueLds<NT> epi;
+    } u;
+};
+
+}  // namespace
+
+// ================================================================================================
+// Scan: pseudo-max, 2-bit scan, keep decision; scan scores and the kept list to the workspace.
+// Grid (S1, Hkv, B); workgroup s1 scans blocks [s1 * bps, (s1 + 1) * bps) of one (sequence, KV
+// head), bps = ceil(nblk / S1) <= kFfdMaxScanBlocks; wave w takes a contiguous quarter of them and
+// keeps kRing blocks in flight.
+// ================================================================================================
+template <int NT>
+__global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
+    __shared__ ScanLds<NT> sm;
+    const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, n = lane & 15;
+    const int G = a.G, hq0 = kvh * G;
+    const size_t bh = (size_t)b * a.Hkv + kvh;
+    const int L = min(max(a.seq_lens[b], 0), a.Lcap);
+    const int nblk = (L + kBlock - 1) / kBlock;
+    const int nblk_cap = a.Lcap / kBlock;
+    const int bps = (nblk + a.S1 - 1) / a.S1;
+    const int jb = min(s * bps, nblk), je = min(jb + bps, nblk);
+    if (jb >= je && !a.mask) {                  // nothing to scan (short sequence), nothing to clear
+        if (tid == 0) a.counts[bh * a.S1 + s] = 0;
+        return;
+    }
+
+    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * 8;
+    const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
+    float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
+
+    // This wave's blocks: [jw0, jw0 + nbw).
+    const int qw_blocks = (bps + kWaves - 1) / kWaves;
+    const int jw0 = min(jb + wave * qw_blocks, je);
+    const int nbw = min(jw0 + qw_blocks, je) - jw0;
+    const int jclamp = nbw > 0 ? jw0 + nbw - 1 : max(je - 1, 0);   // block 0 always exists
+
+    // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
+    // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
+    // draining every load in flight. Order: queries, pseudo-max window blocks, the first ring round.
+    uint32_t qw[NT];
+    load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
+    const int jlast = max(nblk, 1) - 1;
+    const int sink_end = min(a.n_sink, L);
+    const int loc_beg = max(0, L - a.n_local);
+    const int sink_blk_end = (sink_end + kBlock - 1) / kBlock;
+    const int loc_blk_beg = max(loc_beg / kBlock, sink_blk_end);
+    const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
+    auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
+    BlockScan win[kPMW];
+#pragma unroll
+    for (int i = 0; i < kPMW; ++i)
+        win[i] = load_block_scan(codes_bh, absmax_bh, min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
+    BlockScan ring[kRing];
+#pragma unroll
+    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
+
+    HeadConsts<NT> hc;
+    build_query_consts<NT>(sm.qs, qw, G, a.scale, tid, hc);
 
     // ---- pseudo-max over sink and local windows (Eq. 3) ----------------------------------
     float pm[NT];
@@ -249,8 +336,8 @@ __global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
         for (int i = 0; i < kPMW; ++i) {
             const int idx = base + kWaves * i + wave;
             const int j = pm_block(min(idx, npm - 1));
-            float sc[NT][4], M[4];
-            block_scores<NT>(win[i], j, lane, L, hc, sc, M);
+            float sc[NT][4];
+            block_scores<NT>(win[i], j, lane, L, hc, sc);
 #pragma unroll
             for (int T4 = 0; T4 < 4; ++T4) {
                 const int tok = 64 * j + 16 * T4 + n;
@@ -275,7 +362,185 @@ __global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
         thr[t] = m - a.delta;                      // -inf when both windows are empty
     }
 
-    // ---- main loop: scan, decide, and attend kept blocks, per wave ----------------------
+    // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
+    int nkept = 0;                                  // wave-uniform
+    auto decide = [&](const BlockScan& blk, int j) {
+        float sc[NT][4];
+        block_scores<NT>(blk, j, lane, L, hc, sc);
+        uint32_t bits = 0;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3])));
+            const bool keep = hc.live[t] && sig >= thr[t];
+            if (a.mask && n == 0 && hc.live[t])
+                a.mask[((size_t)b * a.Hq + hq0 + 4 * t + g) * nblk_cap + j] = keep ? 1 : 0;
+            const uint64_t bl = __ballot(keep && n == 0);
+            bits |= (uint32_t)(((bl >> 0) & 1u) | ((bl >> 15) & 2u) | ((bl >> 30) & 4u) |
+                               ((bl >> 45) & 8u)) << (4 * t);
+        }
+        if (bits != 0) {                              // wave-uniform: the block is gathered
+            float* sp = shat_bh + (size_t)j * (4 * NT * 64) + lane;
+#pragma unroll
+            for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
+                for (int t = 0; t < NT; ++t) sp[(T4 * NT + t) * 64] = sc[t][T4];
+            if (lane == 0) sm.kept[wave][nkept] = (uint32_t)j | (bits << 24);
+            ++nkept;
+        }
+    };
+    // Every round but the last refills each slot with the block kRing ahead (clamped to the wave's
+    // own last block, which is then still cached); the last round issues no loads, so no wave waits
+    // on a load it does not use.
+    int i0 = 0;
+    for (; i0 + kRing < nbw; i0 += kRing) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+            const int j = jw0 + i0 + r;
+            decide(ring[r], j);
+            ring[r] = load_block_scan(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kRing; ++r)
+        if (i0 + r < nbw) decide(ring[r], jw0 + i0 + r);
+
+    // ---- this workgroup's kept list, in block order, and its length ------------------------
+    if (lane == 0) sm.nkept[wave] = nkept;
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int c = sm.nkept[w];
+        before += w < wave ? c : 0;
+        total += c;
+    }
+    uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap + jb;
+    for (int k = lane; k < nkept; k += 64) list_bh[before + k] = sm.kept[wave][k];
+    if (tid == 0) a.counts[bh * a.S1 + s] = total;
+
+    // Mask entries past the end of the sequence are zero (spread over the scan workgroups).
+    if (a.mask) {
+        for (int j = nblk + s * kThreads + tid; j < nblk_cap; j += a.S1 * kThreads)
+            for (int h = 0; h < G; ++h) a.mask[((size_t)b * a.Hq + hq0 + h) * nblk_cap + j] = 0;
+    }
+}
+
+// ================================================================================================
+// Refinement: Eq. 4 on the kept blocks, online softmax and PV, one partial state per workgroup.
+// Grid (W + B*Hkv). With N kept blocks in all and n_x in KV group x, group x gets
+// W_x = ceil(n_x * min(W, N) / N) workgroups (1 if n_x = 0) in group order; workgroup p of the
+// group refines its kept blocks of rank [p n_x / W_x, (p + 1) n_x / W_x). Workgroups past the last
+// group's exit.
+// ================================================================================================
+template <int NT>
+__global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(RefineArgs a) {
+    __shared__ RefineLds<NT> sm;
+    const int wg = blockIdx.x;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, n = lane & 15;
+    const int G = a.G, S1 = a.S1, npairs = a.npairs;
+
+    // ---- allocation: total kept N, then this workgroup's KV group ---------------------------
+    // One pass reads every scan count (four loads in flight per thread); when they all fit, they
+    // are kept in LDS and summed per KV group with LDS atomics, so nothing is read twice.
+    const int total = npairs * S1;
+    const bool cached = total <= kCountCache && npairs <= kPairChunk;
+    if (cached)
+        for (int i = tid; i < npairs; i += kThreads) sm.pn[i] = 0;
+    __syncthreads();
+    int part = 0;
+    for (int i0 = tid; i0 < total; i0 += 4 * kThreads) {
+        int c[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int idx = i0 + k * kThreads;
+            c[k] = idx < total ? a.counts[idx] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int idx = i0 + k * kThreads;
+            part += c[k];
+            if (cached && idx < total) {
+                sm.cnt[idx] = c[k];
+                if (c[k]) atomicAdd(&sm.pn[idx / S1], c[k]);
+            }
+        }
+    }
+    int N = 0;
+    (void)wg_exclusive_scan(part, sm.wsum, &N);      // its barriers publish cnt and pn
+    const long long Weff = min((long long)a.W, (long long)max(N, 1));
+    int running = 0;
+    for (int c0 = 0; c0 < npairs; c0 += kPairChunk) {
+        const int np = min(kPairChunk, npairs - c0);
+        if (!cached) {                                 // KV groups of this pass, from HBM
+            for (int i = tid; i < np; i += kThreads) sm.pn[i] = 0;
+            __syncthreads();
+            for (int i = tid; i < np * S1; i += kThreads) {
+                const int c = a.counts[(size_t)c0 * S1 + i];
+                if (c) atomicAdd(&sm.pn[i / S1], c);
+            }
+            __syncthreads();
+        }
+        int w4[4], n4[4], sum = 0;                     // thread t: groups c0 + 4t .. c0 + 4t + 3
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int xi = 4 * tid + k;
+            n4[k] = xi < np ? sm.pn[xi] : 0;
+            w4[k] = xi < np ? (n4[k] > 0 ? (int)(((long long)n4[k] * Weff + N - 1) / N) : 1) : 0;
+            sum += w4[k];
+        }
+        int tot = 0;
+        int q0 = running + wg_exclusive_scan(sum, sm.wsum, &tot);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (4 * tid + k < np && wg >= q0 && wg < q0 + w4[k]) {
+                sm.sel[0] = c0 + 4 * tid + k;
+                sm.sel[1] = q0;
+                sm.sel[2] = w4[k];
+                sm.sel[3] = n4[k];
+            }
+            q0 += w4[k];
+        }
+        running += tot;
+        if (!cached) __syncthreads();                  // pn is rewritten by the next pass
+    }
+    if (wg >= running) return;                      // uniform: beyond the last group's workgroups
+    __syncthreads();
+    const int x = sm.sel[0], Qx = sm.sel[1], Wx = sm.sel[2], nx = sm.sel[3];
+    const int b = x / a.Hkv, kvh = x % a.Hkv, hq0 = kvh * G;
+    const int p = wg - Qx;
+    const int r0 = (int)((long long)p * nx / Wx), r1 = (int)((long long)(p + 1) * nx / Wx);
+    const size_t bh = (size_t)x;
+    const int L = min(max(a.seq_lens[b], 0), a.Lcap);
+    const int nblk = (L + kBlock - 1) / kBlock;
+    const int nblk_cap = a.Lcap / kBlock;
+    const int bps = (nblk + S1 - 1) / S1;
+    const int last_row = max(L, 1) - 1;
+    if (p == 0 && tid == 0) a.table[x] = make_int2(Qx, Wx);
+
+    const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
+    const int8_t* resid_bh = a.resid + bh * (size_t)a.Lcap * kD;
+    const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
+    const float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
+    const uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap;
+
+    uint32_t qw[NT];
+    load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
+    // exclusive prefix of the group's per-split counts: rank r lies in split s with
+    // pref[s] <= r < pref[s + 1], at list position s * bps + r - pref[s]
+    int run = 0;
+    for (int c0 = 0; c0 < S1; c0 += kThreads) {
+        const int sidx = c0 + tid;
+        const int c = sidx < S1 ? (cached ? sm.cnt[x * S1 + sidx] : a.counts[bh * S1 + sidx]) : 0;
+        int tot = 0;
+        const int e = wg_exclusive_scan(c, sm.wsum, &tot);
+        if (sidx < S1) sm.pref[sidx] = run + e;
+        run += tot;
+    }
+    if (tid == 0) sm.pref[S1] = run;
+    __syncthreads();
+    HeadConsts<NT> hc;                              // built once the share's list loads are issued
+
     PvAcc<NT> pv;
     pv.zero();
     float m_run[NT], l_part[NT];
@@ -283,96 +548,70 @@ __global__ __launch_bounds__(kThreads, 2) void ffd_decode_kernel(DecodeArgs a) {
     for (int t = 0; t < NT; ++t) { m_run[t] = -INFINITY; l_part[t] = 0.f; }
     TileP<NT>& tp = sm.tp[wave];
 
-    // refine (Eq. 4) and attend one tile of a parked block from its fetched residual and values
-    auto attend_tile = [&](const TileGather& tg, const Parked<NT>& pk, int T4) {
+    // refine (Eq. 4) and attend tile `wave` of one kept block
+    auto attend = [&](const RefineTile<NT>& rt, uint32_t bits) {
         float z[NT];
         bool keep[NT];
-        const float Mt = pk.M[T4][n];
+        const float Mt = bf16_to_f32((uint16_t)rt.m);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             v4i acc = {0, 0, 0, 0};
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], tg.r0, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], tg.r1, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], rt.r0, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], rt.r1, acc, 0, 0, 0);
             const float R = fmaf(65536.f, (float)acc.z, fmaf(256.f, (float)acc.y, (float)acc.x));
-            const float sct = pk.sc[T4][t][lane];
+            const float sct = rt.sc[t];
             z[t] = sct == -INFINITY ? -INFINITY : fmaf(R, Mt * hc.kap2[t], sct);
-            keep[t] = (pk.keep >> (4 * t + g)) & 1u;
+            keep[t] = (bits >> (4 * t + g)) & 1u;
         }
         softmax_tile<NT>(z, keep, m_run, l_part, tp, g, n);
         wave_lds_fence();
-        pv_tile<NT>(pv, tp, tg.vt);
+        pv_tile<NT>(pv, tp, rt.vt);
         wave_lds_fence();
     };
 
-    for (int i0 = 0; jb + kWaves * i0 + wave < je; i0 += kRing) {
-        int parked = 0;                                       // wave-uniform
+    bool consts_ready = false;
+    for (int c = r0; c < r1; c += kChunk) {
+        const int m = min(kChunk, r1 - c);
+        for (int i = tid; i < m; i += kThreads) {
+            const int r = c + i;
+            int lo = 0, hi = S1;                    // largest split with pref[split] <= r
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (sm.pref[mid] <= r) lo = mid; else hi = mid;
+            }
+            sm.u.list[i] = list_bh[lo * bps + (r - sm.pref[lo])];
+        }
+        if (!consts_ready) {                        // the query loads and the list loads overlap
+            build_query_consts<NT>(sm.qs, qw, G, a.scale, tid, hc);
+            consts_ready = true;
+        }
+        __syncthreads();
+        auto block_of = [&](int i) { return (int)(sm.u.list[min(i, m - 1)] & 0xffffffu); };
+        RefineTile<NT> ring[kRefineRing];
 #pragma unroll
-        for (int r = 0; r < kRing; ++r) {
-            const int j = jb + kWaves * (i0 + r) + wave;      // wave-uniform
-            if (j < je) {
-                float sc[NT][4], M[4];
-                block_scores<NT>(ring[r], j, lane, L, hc, sc, M);
-                ring[r] = load_block_scan(codes_bh, absmax_bh, min(j + kWaves * kRing, jlast), lane);
-                bool keep[NT], any = false;
+        for (int r = 0; r < kRefineRing; ++r)
+            ring[r] = load_refine_tile<NT>(resid_bh, v_bh, shat_bh, absmax_bh, block_of(r), wave, lane, last_row);
+        // the refill of the last round re-reads the share's last tile (clamped): it is still
+        // cached, and a conditional refill would cost more registers than it saves
+        for (int i0 = 0; i0 < m; i0 += kRefineRing) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3])));
-                    keep[t] = hc.live[t] && sig >= thr[t];
-                    any |= keep[t];
-                    if (a.mask && n == 0 && hc.live[t])
-                        a.mask[((size_t)b * a.Hq + hq0 + 4 * t + g) * nblk_cap + j] = keep[t] ? 1 : 0;
-                }
-                if (__ballot(any) != 0) {                   // some head of the group keeps block j
-                    uint32_t bits = 0;
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const uint64_t bl = __ballot(keep[t] && n == 0);
-                        bits |= (uint32_t)(((bl >> 0) & 1u) | ((bl >> 15) & 2u) | ((bl >> 30) & 4u) |
-                                           ((bl >> 45) & 8u)) << (4 * t);
-                    }
-                    Parked<NT>& pk = sm.park[wave][parked];
-#pragma unroll
-                    for (int T4 = 0; T4 < 4; ++T4) {
-#pragma unroll
-                        for (int t = 0; t < NT; ++t) pk.sc[T4][t][lane] = sc[t][T4];
-                        if (g == 0) pk.M[T4][n] = M[T4];
-                    }
-                    if (lane == 0) {
-                        pk.j = j;
-                        pk.keep = bits;
-                    }
-                    ++parked;
-                }
+            for (int r = 0; r < kRefineRing; ++r) {
+                const int i = i0 + r;
+                if (i < m) attend(ring[r], sm.u.list[i] >> 24);
+                ring[r] = load_refine_tile<NT>(resid_bh, v_bh, shat_bh, absmax_bh,
+                                               block_of(i + kRefineRing), wave, lane, last_row);
             }
         }
-        if (parked == 0) continue;
-        wave_lds_fence();
-        // attend the parked blocks' tiles k = 4e + T4 in pairs, two tiles in flight; the pair loop
-        // is not unrolled, so the tile code exists twice and the register budget stays bounded
-        const int ntile = 4 * parked;
-        auto tile_of = [&](int k) { return 4 * sm.park[wave][k >> 2].j + (k & 3); };
-        TileGather g0 = load_tile_gather(resid_bh, v_bh, tile_of(0), lane, L);
-        TileGather g1 = load_tile_gather(resid_bh, v_bh, tile_of(1), lane, L);
-#pragma unroll 1
-        for (int k = 0; k < ntile; k += 2) {
-            attend_tile(g0, sm.park[wave][k >> 2], k & 3);
-            g0 = load_tile_gather(resid_bh, v_bh, tile_of(min(k + 2, ntile - 1)), lane, L);
-            attend_tile(g1, sm.park[wave][(k + 1) >> 2], (k + 1) & 3);
-            g1 = load_tile_gather(resid_bh, v_bh, tile_of(min(k + 3, ntile - 1)), lane, L);
-        }
+        __syncthreads();                // the list is rewritten by the next chunk / the epilogue
     }
 
-    write_partials<NT>(sm.epi, pv, m_run, l_part, wave, lane, G, hq0, a.Hq, a.S, b, s, a.part_m,
+    write_partials<NT>(sm.u.epi, pv, m_run, l_part, wave, lane, G, (size_t)wg * G, 1, a.part_m,
                        a.part_l, a.part_acc);
-
-    // Mask entries past the end of the sequence are zero (spread over the splits).
-    if (a.mask) {
-        for (int j = nblk + s * kThreads + tid; j < nblk_cap; j += a.S * kThreads)
-            for (int h = 0; h < G; ++h) a.mask[((size_t)b * a.Hq + hq0 + h) * nblk_cap + j] = 0;
-    }
 }
 
-template __global__ void ffd_decode_kernel<1>(DecodeArgs);
-template __global__ void ffd_decode_kernel<2>(DecodeArgs);
+template __global__ void ffd_scan_kernel<1>(ScanArgs);
+template __global__ void ffd_scan_kernel<2>(ScanArgs);
+template __global__ void ffd_refine_kernel<1>(RefineArgs);
+template __global__ void ffd_refine_kernel<2>(RefineArgs);
 
 }  // namespace ffd

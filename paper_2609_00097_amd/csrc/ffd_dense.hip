@@ -102,8 +102,8 @@ __global__ __launch_bounds__(kThreads, NT == 1 ? 4 : 2) void dense_decode_kernel
         vc = vn;
     }
 
-    write_partials<NT>(sm.epi, pv, m_run, l_part, wave, lane, G, hq0, a.Hq, a.S, b, s, a.part_m,
-                       a.part_l, a.part_acc);
+    write_partials<NT>(sm.epi, pv, m_run, l_part, wave, lane, G, ((size_t)b * a.Hq + hq0) * a.S + s,
+                       (size_t)a.S, a.part_m, a.part_l, a.part_acc);
 }
 
 template __global__ void dense_decode_kernel<1>(DenseArgs);

@@ -164,7 +164,8 @@ __device__ __forceinline__ void softmax_tile(const float (&z)[NT], const bool (&
     }
 }
 
-// Workgroup epilogue: combine the four waves' (m, l, acc) and write this split's partial state.
+// Workgroup epilogue: combine the four waves' (m, l, acc) and write one partial state per head.
+// Head h (0 <= h < G) of the group goes to partial row row0 + h * head_stride.
 template <int NT>
 struct EpilogueLds {
     float m[kWaves][4 * NT];
@@ -175,9 +176,8 @@ struct EpilogueLds {
 template <int NT>
 __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<NT>& pv,
                                                const float (&m_run)[NT], const float (&l_part)[NT],
-                                               int wave, int lane, int G, int hq0, int Hq, int S,
-                                               int b, int s, float* part_m, float* part_l,
-                                               float* part_acc) {
+                                               int wave, int lane, int G, size_t row0, size_t head_stride,
+                                               float* part_m, float* part_l, float* part_acc) {
     const int g = lane >> 4, n = lane & 15;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -208,7 +208,7 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
                 }
             }
         }
-        const size_t row = ((size_t)b * Hq + hq0 + h) * S + s;
+        const size_t row = row0 + (size_t)h * head_stride;
         part_acc[row * kD + d] = a;
         if (d == 0) {
             part_m[row] = mx;

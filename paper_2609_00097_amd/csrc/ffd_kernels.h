@@ -6,20 +6,42 @@
 
 namespace ffd {
 
-struct DecodeArgs {
+// Kept-block list entries staged in LDS per pass of the refinement kernel.
+constexpr int kFfdChunk = 1024;
+// Most blocks one scan workgroup covers (its kept list is staged in LDS), most scan workgroups per
+// (sequence, KV head).
+constexpr int kFfdMaxScanBlocks = 256;
+constexpr int kFfdMaxScanSplits = 1024;
+
+struct ScanArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
-    const uint32_t* codes;      // [B, Hkv, Lcap/16, 64, 2]
-    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap]
+    const uint32_t* codes;      // [B, Hkv, Lcap/64, 64, 8]
+    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
+    const int32_t* seq_lens;    // [B]
+    uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, per scan split
+    int* counts;                // [B*Hkv, S1]: kept blocks per scan split
+    float* shat;                // [B, Hkv, Lcap/64, 4, NT, 64]: scan scores of kept blocks
+    uint8_t* mask;              // [B, Hq, Lcap/64] or null
+    int Hq, Hkv, Lcap, G, S1;
+    float delta, scale;
+    int n_sink, n_local;
+};
+
+struct RefineArgs {
+    const uint16_t* q;          // bf16 [B, Hq, 128]
+    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
     const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]
     const uint16_t* v;          // bf16 [B, Hkv, Lcap, 128]
     const int32_t* seq_lens;    // [B]
-    float* part_m;              // [B, Hq, S]
-    float* part_l;              // [B, Hq, S]
-    float* part_acc;            // [B, Hq, S, 128]
-    uint8_t* mask;              // [B, Hq, Lcap/64] or null
-    int Hq, Hkv, Lcap, G, S;
-    float delta, scale;
-    int n_sink, n_local;
+    const uint32_t* lists;      // written by ffd_scan_kernel
+    const int* counts;          // written by ffd_scan_kernel
+    const float* shat;          // written by ffd_scan_kernel
+    int2* table;                // [B*Hkv]: (first workgroup, workgroups) of each KV group
+    float* part_m;              // [(W + B*Hkv) * G]
+    float* part_l;
+    float* part_acc;            // [(W + B*Hkv) * G, 128]
+    int Hq, Hkv, Lcap, G, S1, W, npairs;
+    float scale;
 };
 
 struct DenseArgs {
@@ -42,10 +64,11 @@ struct QuantArgs {
     int Hkv, Lcap, t_begin, t_end;
 };
 
-template <int NT> __global__ void ffd_decode_kernel(DecodeArgs a);
+template <int NT> __global__ void ffd_scan_kernel(ScanArgs a);
+template <int NT> __global__ void ffd_refine_kernel(RefineArgs a);
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
 __global__ void quantize_keys_kernel(QuantArgs a);
 __global__ void lse_merge_kernel(const float* part_m, const float* part_l, const float* part_acc, int S,
-                                 uint16_t* out, float* lse);
+                                 const int2* table, int G, uint16_t* out, float* lse);
 
 }  // namespace ffd

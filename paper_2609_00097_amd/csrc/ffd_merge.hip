@@ -3,6 +3,10 @@
 // lse = M* + ln l*. Splits that kept nothing carry m = -inf and are skipped; a head with no split
 // gets out = 0 and lse = -inf.
 //
+// Partial rows of head bh = b * Hq + h: without a table, rows bh * S + s for s < S (the dense path's
+// fixed splits); with a table (the FFD path), rows (first + i) * G + bh % G for i < count, where
+// (first, count) = table[bh / G] describes the refinement workgroups given to that KV group.
+//
 // Mapping: one workgroup per (sequence, query head); thread (d4, r) folds the splits s = r (mod 8)
 // of dims 4*d4..4*d4+3 into an online (max, sum, acc) with 8 float4 loads in flight, then the
 // 8 threads of a d4 combine with shuffles.
@@ -32,8 +36,15 @@ __device__ __forceinline__ void lse_fold(float& M, float& l, float4& acc, float 
 __global__ __launch_bounds__(kThreads) void lse_merge_kernel(const float* __restrict__ part_m,
                                                              const float* __restrict__ part_l,
                                                              const float* __restrict__ part_acc, int S,
+                                                             const int2* __restrict__ table, int G,
                                                              uint16_t* __restrict__ out, float* __restrict__ lse) {
-    const size_t row0 = (size_t)blockIdx.x * S;      // blockIdx.x = b * Hq + h
+    size_t row0 = (size_t)blockIdx.x * S, stride = 1;      // blockIdx.x = b * Hq + h
+    if (table) {
+        const int2 fc = table[blockIdx.x / G];
+        row0 = (size_t)fc.x * G + blockIdx.x % G;
+        stride = (size_t)G;
+        S = fc.y;
+    }
     const int d4 = threadIdx.x / kMergeLanes, r = threadIdx.x % kMergeLanes;
     float M = -INFINITY, l = 0.f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -48,9 +59,10 @@ __global__ __launch_bounds__(kThreads) void lse_merge_kernel(const float* __rest
             ls[u] = 0.f;
             as[u] = make_float4(0.f, 0.f, 0.f, 0.f);
             if (s < S) {
-                ms[u] = part_m[row0 + s];
-                ls[u] = part_l[row0 + s];
-                as[u] = *reinterpret_cast<const float4*>(part_acc + (row0 + s) * kD + 4 * d4);
+                const size_t row = row0 + (size_t)s * stride;
+                ms[u] = part_m[row];
+                ls[u] = part_l[row];
+                as[u] = *reinterpret_cast<const float4*>(part_acc + row * kD + 4 * d4);
             }
         }
 #pragma unroll

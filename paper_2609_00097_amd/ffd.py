@@ -21,8 +21,9 @@ MAX_SPLITS = 1024
 STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
           3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
 
-EXPORTS = ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
-           "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_status_string")
+EXPORTS = ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+           "ffd_dense_decode_attention",
+           "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
 
 class FfdLibraryError(RuntimeError):
@@ -55,14 +56,16 @@ def lib() -> ctypes.CDLL:
     so.ffd_quantize_keys.argtypes = [P, P, P, P, I, I, I, I, I, I, P]
     so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, I, I, F,
                                         P, P, P, P, SZ, P]
+    so.ffd_decode_attention_events.argtypes = so.ffd_decode_attention.argtypes + [P]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
     so.ffd_resolve_splits.argtypes = [I, I, I, I]
-    so.ffd_workspace_bytes.argtypes = [I, I, I, I, I, I]
-    so.ffd_workspace_bytes.restype = SZ
+    for name in ("ffd_workspace_bytes", "ffd_dense_workspace_bytes"):
+        getattr(so, name).argtypes = [I, I, I, I, I, I]
+        getattr(so, name).restype = SZ
     so.ffd_status_string.argtypes = [I]
     so.ffd_status_string.restype = ctypes.c_char_p
-    for name in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
-                 "ffd_resolve_splits"):
+    for name in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+                 "ffd_dense_decode_attention", "ffd_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
     return so
@@ -96,14 +99,19 @@ def resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
     return lib().ffd_resolve_splits(B, Hkv, Lcap, num_splits)
 
 
-def workspace_bytes(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
-    return lib().ffd_workspace_bytes(B, Hq, Hkv, Lcap, HEAD_DIM, num_splits)
+def workspace_bytes(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0,
+                    dense: bool = False) -> int:
+    """Bytes for ``decode_attention`` (enough for both entry points), or for the dense one only."""
+    fn = lib().ffd_dense_workspace_bytes if dense else lib().ffd_workspace_bytes
+    return fn(B, Hq, Hkv, Lcap, HEAD_DIM, num_splits)
 
 
-def new_workspace(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0, device="cuda"):
-    """A workspace for either attention entry point (one per stream)."""
-    return torch.empty(max(workspace_bytes(B, Hq, Hkv, Lcap, num_splits), 16), dtype=torch.uint8,
-                       device=device)
+def new_workspace(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0, device="cuda",
+                  dense: bool = False):
+    """A workspace (one per stream): for ``decode_attention`` and the dense entry point alike, or,
+    with ``dense=True``, the smaller one the dense entry point needs."""
+    return torch.empty(max(workspace_bytes(B, Hq, Hkv, Lcap, num_splits, dense), 16),
+                       dtype=torch.uint8, device=device)
 
 
 def quantized_shapes(B: int, Hkv: int, Lcap: int):
@@ -147,8 +155,12 @@ def _attn_outputs(q, B, Hq, Lcap, want_lse, want_mask, out, lse, mask):
 def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_sink: int = 64,
                      n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
                      return_lse: bool = True, return_mask: bool = False, workspace=None,
-                     out=None, lse=None, mask=None):
-    """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested)."""
+                     out=None, lse=None, mask=None, stage_events=None):
+    """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested).
+
+    ``stage_events``: optional four ``torch.cuda.Event`` objects, already recorded once (so that
+    they exist), which the library records before the scan kernel, after it, after the refinement
+    kernel and after the merge."""
     B, Hq, D = q.shape
     Hkv, Lcap = v.shape[1], v.shape[2]
     _need(q, "q", torch.bfloat16)
@@ -161,11 +173,16 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
                                    return_mask or mask is not None, out, lse, mask)
     if workspace is None:
         workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device)
-    _check("ffd_decode_attention", lib().ffd_decode_attention(
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != 4 or any(e.cuda_event == 0 for e in stage_events):
+            raise ValueError("stage_events must be four recorded torch.cuda.Event objects")
+        ev = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
+    _check("ffd_decode_attention", lib().ffd_decode_attention_events(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
         D, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
         _ptr(lse), _ptr(mask), _ptr(workspace), workspace.numel() * workspace.element_size(),
-        _stream(q.device)))
+        _stream(q.device), ev))
     return out, lse, mask
 
 
@@ -180,7 +197,7 @@ def dense_decode_attention(q, k, v, seq_lens, *, num_splits: int = 0, softmax_sc
     _need(seq_lens, "seq_lens", torch.int32, (B,))
     out, lse, _ = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None, False, out, lse, None)
     if workspace is None:
-        workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device)
+        workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device, dense=True)
     _check("ffd_dense_decode_attention", lib().ffd_dense_decode_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap, D, num_splits,
         float(softmax_scale), _ptr(out), _ptr(lse), _ptr(workspace),

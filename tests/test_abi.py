@@ -25,8 +25,9 @@ def so():
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_dense_decode_attention",
-              "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_status_string"):
+    for n in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+              "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes",
+              "ffd_status_string"):
         assert n in names
 
 
@@ -42,12 +43,23 @@ def test_status_strings(so):
 
 
 def test_splits_and_workspace_sizes(so):
-    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 64
+    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 16           # about 512 workgroups
     assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
-    assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 64 * 130 * 4
+    # partials (S*P + P)*G*(D+2)*4 | table P*8 | counts P*S1*4 | lists P*C*4 | scores P*C*1024*NT,
+    # each region on a 256-byte boundary (S1 = 32 scan splits at 4 x 8 x 128K, 4 at 1 x 2 x 4K)
+    up = lambda x: -(-x // 256) * 256
+    P, G, C = 32, 4, 2048
+    assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
+        up((16 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 32 * 4) + up(P * C * 4) + P * C * 1024)
+    P, G, C = 2, 8, 64
+    assert so.ffd_workspace_bytes(1, 16, 2, 4096, 128, 3) == (
+        up((3 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 4 * 4) + up(P * C * 4) + P * C * 2048)
+    assert so.ffd_workspace_bytes(1, 8, 8, 1 << 25, 128, 1) == 0         # Lcap beyond 2^24 tokens
+    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 16 * 130 * 4
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
+    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
 
 
 def _decode(so, **kw):
@@ -73,6 +85,10 @@ def test_misaligned_and_small_workspace(so):
     args = dict(q=fake, codes=fake, absmax=fake, resid=fake, v=fake, lens=fake, out=fake, ws=fake)
     assert _decode(so, **args, ws_bytes=16) == 3
     assert _decode(so, **{**args, "q": fake + 2}, ws_bytes=1 << 30) == 1
+    # the dense entry point needs only the partials
+    need = so.ffd_dense_workspace_bytes(1, 32, 8, 4096, 128, 0)
+    assert so.ffd_dense_decode_attention(fake, fake, fake, fake, 1, 32, 8, 4096, 128, 0, 0.0, fake, None,
+                                         fake, need - 1, None) == 3
 
 
 def test_quantize_range_checks(so):

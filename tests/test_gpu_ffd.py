@@ -130,6 +130,24 @@ def test_one_workspace_serves_repeated_and_alternating_calls():
         assert torch.equal(dout, dref_out) and torch.equal(dlse, dref_lse)
 
 
+def test_stage_events_time_the_three_kernels_without_changing_results():
+    from paper_2609_00097_amd import ffd
+    c = I.small_case(seed=67, B=2, Hq=8, Hkv=2, seq_lens=(3000, 1200), heavy_frac=0.05)
+    up = Uploaded(c)
+    qk = _quant(up)
+    ref_out, ref_lse, _ = _ffd(up, qk, 5.0)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in evs:
+        e.record()
+    out, lse, _ = ffd.decode_attention(up.q, *qk, up.v, up.seq_lens, delta=5.0, stage_events=evs)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref_out) and torch.equal(lse, ref_lse)
+    stages = [evs[i].elapsed_time(evs[i + 1]) for i in range(3)]
+    assert all(t > 0 for t in stages), stages
+    with pytest.raises(ValueError):
+        ffd.decode_attention(up.q, *qk, up.v, up.seq_lens, delta=5.0, stage_events=evs[:3])
+
+
 def test_argument_errors_return_status_without_launch():
     from paper_2609_00097_amd import ffd
     c = I.small_case(seed=1, B=1, Hq=8, Hkv=2, seq_lens=(100,))
