@@ -68,7 +68,10 @@ int head_tiles(int G) { return G <= 4 ? 1 : 2; }
 // Workgroups of the scan kernel per (sequence, KV head): about kScanWorkgroups in all, each scanning
 // at least kMinScanBlocks blocks so the pseudo-max and query setup stay a small part of its work, and
 // at most kFfdMaxScanBlocks (its kept list is staged in LDS).
-constexpr int kScanWorkgroups = 1024;
+#ifndef FFD_SCAN_WGS
+#define FFD_SCAN_WGS 1024
+#endif
+constexpr int kScanWorkgroups = FFD_SCAN_WGS;
 constexpr int kMinScanBlocks = 16;
 
 int scan_splits(int B, int Hkv, int Lcap) {
@@ -215,6 +218,7 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
     auto mark = [&](int i) {
         return stage_events && hipEventRecord(stage_events[i], stream) != hipSuccess ? FFD_ERR_HIP : FFD_OK;
     };
+
     if ((st = mark(0)) != FFD_OK) return st;
     if (G <= 4)
         hipLaunchKernelGGL(ffd_scan_kernel<1>, scan_grid, dim3(kThreads), 0, stream, sa);

@@ -222,7 +222,9 @@ __device__ __forceinline__ RefineTile<NT> load_refine_tile(const int8_t* __restr
     return r;
 }
 
-// Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum.
+// Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum. One
+// barrier: consecutive calls must alternate between the two halves of wsum[2][kWaves] (a wave
+// reaching call k + 2 has passed call k + 1's barrier, so every wave has read call k's half).
 __device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = x;
@@ -240,7 +242,6 @@ __device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
         before += w < wave ? s : 0;
         tot += s;
     }
-    __syncthreads();
     *total = tot;
     return before + incl - x;
 }
@@ -251,11 +252,11 @@ constexpr int kCountCache = 4096;            // scan counts kept in LDS when the
 template <int NT>
 struct RefineLds {
     QueryLds<NT> qs;
-    int wsum[kWaves];
+    int wsum[2][kWaves];                 // wg_exclusive_scan scratch, alternating halves
     int sel[4];                          // this workgroup's KV group: pair, first workgroup, workgroups, kept
-    int pn[kPairChunk];                  // kept blocks per KV group of the current pass
-    int cnt[kCountCache];                // all scan counts, when they fit
-    int pref[kFfdMaxScanSplits + 1];     // exclusive prefix of the group's per-scan-split kept counts
+    int pn[kPairChunk];                  // kept blocks per KV group of the current pass (large inputs)
+    int cnt[kCountCache + 1];            // exclusive prefix of all scan counts, when they fit
+    int pref[kFfdMaxScanSplits + 1];     // exclusive prefix of the group's per-split counts (large inputs)
     TileP<NT> tp[kWaves];
     union {
         uint32_t list[kChunk];           // kept blocks of the share: j | keep bits << 24
@@ -441,38 +442,72 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const int G = a.G, S1 = a.S1, npairs = a.npairs;
 
     // ---- allocation: total kept N, then this workgroup's KV group ---------------------------
-    // One pass reads every scan count (four loads in flight per thread); when they all fit, they
-    // are kept in LDS and summed per KV group with LDS atomics, so nothing is read twice.
+    // Usual case: all scan counts fit in LDS. Thread t loads counts [16t, 16t + 16) and one
+    // workgroup scan gives their exclusive prefix in (group, split) order, so N, every group's
+    // n_x and the group's split prefix all come from LDS. Otherwise the counts are summed per
+    // group in passes of kPairChunk groups with LDS atomics.
     const int total = npairs * S1;
     const bool cached = total <= kCountCache && npairs <= kPairChunk;
-    if (cached)
-        for (int i = tid; i < npairs; i += kThreads) sm.pn[i] = 0;
-    __syncthreads();
-    int part = 0;
-    for (int i0 = tid; i0 < total; i0 += 4 * kThreads) {
-        int c[4];
+    int N = 0, running = 0, half = 0;
+    auto scan = [&](int v, int* tot) {
+        const int e = wg_exclusive_scan(v, sm.wsum[half], tot);
+        half ^= 1;
+        return e;
+    };
+    const long long W = a.W;
+    auto alloc = [&](int nx, long long Weff) {
+        return nx > 0 ? (int)(((long long)nx * Weff + N - 1) / N) : 1;
+    };
+    if (cached) {
+        const int i0 = 16 * tid;
+        int c[16], sum = 0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int idx = i0 + k * kThreads;
-            c[k] = idx < total ? a.counts[idx] : 0;
+        for (int k = 0; k < 16; k += 4) {
+            // the counts region is padded to 256 bytes, so the last int4 stays inside it
+            int4 v = make_int4(0, 0, 0, 0);
+            if (i0 + k < total) v = *reinterpret_cast<const int4*>(a.counts + i0 + k);
+            c[k] = v.x; c[k + 1] = v.y; c[k + 2] = v.z; c[k + 3] = v.w;
         }
 #pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            if (i0 + k >= total) c[k] = 0;
+            sum += c[k];
+        }
+        int run = scan(sum, &N);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            if (i0 + k < total) sm.cnt[i0 + k] = run;
+            run += c[k];
+        }
+        if (tid == 0) sm.cnt[total] = N;
+        __syncthreads();
+        const long long Weff = min(W, (long long)max(N, 1));
+        int w4[4], n4[4], s4 = 0;                      // thread t: groups 4t .. 4t + 3
+#pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int idx = i0 + k * kThreads;
-            part += c[k];
-            if (cached && idx < total) {
-                sm.cnt[idx] = c[k];
-                if (c[k]) atomicAdd(&sm.pn[idx / S1], c[k]);
+            const int xi = 4 * tid + k;
+            n4[k] = xi < npairs ? sm.cnt[(xi + 1) * S1] - sm.cnt[xi * S1] : 0;
+            w4[k] = xi < npairs ? alloc(n4[k], Weff) : 0;
+            s4 += w4[k];
+        }
+        int q0 = scan(s4, &running);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (4 * tid + k < npairs && wg >= q0 && wg < q0 + w4[k]) {
+                sm.sel[0] = 4 * tid + k;
+                sm.sel[1] = q0;
+                sm.sel[2] = w4[k];
+                sm.sel[3] = n4[k];
             }
+            q0 += w4[k];
         }
-    }
-    int N = 0;
-    (void)wg_exclusive_scan(part, sm.wsum, &N);      // its barriers publish cnt and pn
-    const long long Weff = min((long long)a.W, (long long)max(N, 1));
-    int running = 0;
-    for (int c0 = 0; c0 < npairs; c0 += kPairChunk) {
-        const int np = min(kPairChunk, npairs - c0);
-        if (!cached) {                                 // KV groups of this pass, from HBM
+    } else {
+        int part = 0;
+        for (int i = tid; i < total; i += kThreads) part += a.counts[i];
+        (void)scan(part, &N);
+        const long long Weff = min(W, (long long)max(N, 1));
+        for (int c0 = 0; c0 < npairs; c0 += kPairChunk) {
+            const int np = min(kPairChunk, npairs - c0);
             for (int i = tid; i < np; i += kThreads) sm.pn[i] = 0;
             __syncthreads();
             for (int i = tid; i < np * S1; i += kThreads) {
@@ -480,29 +515,29 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                 if (c) atomicAdd(&sm.pn[i / S1], c);
             }
             __syncthreads();
-        }
-        int w4[4], n4[4], sum = 0;                     // thread t: groups c0 + 4t .. c0 + 4t + 3
+            int w4[4], n4[4], s4 = 0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int xi = 4 * tid + k;
-            n4[k] = xi < np ? sm.pn[xi] : 0;
-            w4[k] = xi < np ? (n4[k] > 0 ? (int)(((long long)n4[k] * Weff + N - 1) / N) : 1) : 0;
-            sum += w4[k];
-        }
-        int tot = 0;
-        int q0 = running + wg_exclusive_scan(sum, sm.wsum, &tot);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            if (4 * tid + k < np && wg >= q0 && wg < q0 + w4[k]) {
-                sm.sel[0] = c0 + 4 * tid + k;
-                sm.sel[1] = q0;
-                sm.sel[2] = w4[k];
-                sm.sel[3] = n4[k];
+            for (int k = 0; k < 4; ++k) {
+                const int xi = 4 * tid + k;
+                n4[k] = xi < np ? sm.pn[xi] : 0;
+                w4[k] = xi < np ? alloc(n4[k], Weff) : 0;
+                s4 += w4[k];
             }
-            q0 += w4[k];
+            int tot = 0;
+            int q0 = running + scan(s4, &tot);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if (4 * tid + k < np && wg >= q0 && wg < q0 + w4[k]) {
+                    sm.sel[0] = c0 + 4 * tid + k;
+                    sm.sel[1] = q0;
+                    sm.sel[2] = w4[k];
+                    sm.sel[3] = n4[k];
+                }
+                q0 += w4[k];
+            }
+            running += tot;
+            __syncthreads();                           // pn is rewritten by the next pass
         }
-        running += tot;
-        if (!cached) __syncthreads();                  // pn is rewritten by the next pass
     }
     if (wg >= running) return;                      // uniform: beyond the last group's workgroups
     __syncthreads();
@@ -527,18 +562,22 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     uint32_t qw[NT];
     load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
     // exclusive prefix of the group's per-split counts: rank r lies in split s with
-    // pref[s] <= r < pref[s + 1], at list position s * bps + r - pref[s]
-    int run = 0;
-    for (int c0 = 0; c0 < S1; c0 += kThreads) {
-        const int sidx = c0 + tid;
-        const int c = sidx < S1 ? (cached ? sm.cnt[x * S1 + sidx] : a.counts[bh * S1 + sidx]) : 0;
-        int tot = 0;
-        const int e = wg_exclusive_scan(c, sm.wsum, &tot);
-        if (sidx < S1) sm.pref[sidx] = run + e;
-        run += tot;
+    // pref(s) <= r < pref(s + 1), at list position s * bps + r - pref(s)
+    if (!cached) {
+        int run = 0;
+        for (int c0 = 0; c0 < S1; c0 += kThreads) {
+            const int sidx = c0 + tid;
+            const int c = sidx < S1 ? a.counts[bh * S1 + sidx] : 0;
+            int tot = 0;
+            const int e = scan(c, &tot);
+            if (sidx < S1) sm.pref[sidx] = run + e;
+            run += tot;
+        }
+        if (tid == 0) sm.pref[S1] = run;
+        __syncthreads();
     }
-    if (tid == 0) sm.pref[S1] = run;
-    __syncthreads();
+    const int* pref = cached ? sm.cnt + x * S1 : sm.pref;
+    const int pref0 = cached ? pref[0] : 0;
     HeadConsts<NT> hc;                              // built once the share's list loads are issued
 
     PvAcc<NT> pv;
@@ -574,12 +613,12 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         const int m = min(kChunk, r1 - c);
         for (int i = tid; i < m; i += kThreads) {
             const int r = c + i;
-            int lo = 0, hi = S1;                    // largest split with pref[split] <= r
+            int lo = 0, hi = S1;                    // largest split with pref(split) <= r
             while (hi - lo > 1) {
                 const int mid = (lo + hi) >> 1;
-                if (sm.pref[mid] <= r) lo = mid; else hi = mid;
+                if (pref[mid] - pref0 <= r) lo = mid; else hi = mid;
             }
-            sm.u.list[i] = list_bh[lo * bps + (r - sm.pref[lo])];
+            sm.u.list[i] = list_bh[lo * bps + (r - (pref[lo] - pref0))];
         }
         if (!consts_ready) {                        // the query loads and the list loads overlap
             build_query_consts<NT>(sm.qs, qw, G, a.scale, tid, hc);
@@ -608,6 +647,8 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     write_partials<NT>(sm.u.epi, pv, m_run, l_part, wave, lane, G, (size_t)wg * G, 1, a.part_m,
                        a.part_l, a.part_acc);
 }
+
+
 
 template __global__ void ffd_scan_kernel<1>(ScanArgs);
 template __global__ void ffd_scan_kernel<2>(ScanArgs);

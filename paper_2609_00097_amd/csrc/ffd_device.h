@@ -217,4 +217,70 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
     }
 }
 
+// Log-sum-exp merge of `count` partial rows row0 + i * stride (i < count) of one head into its bf16
+// output row and lse (Sec. 2, flash-decoding): M* = max m_i, l* = sum e^{m_i - M*} l_i,
+// out = sum e^{m_i - M*} acc_i / l*, lse = M* + ln l*. Rows with m = -inf are skipped; no row
+// gives out = 0, lse = -inf. Run by all 256 threads of a workgroup: thread (d4, r) folds rows
+// i = r (mod 8) of dims 4*d4 .. 4*d4 + 3 with 8 float4 loads in flight, then the 8 threads of a
+// d4 combine with shuffles.
+constexpr int kMergeLanes = 8;
+
+__device__ __forceinline__ void lse_fold(float& M, float& l, float4& acc, float m2, float l2, float4 a2) {
+    const float mn = fmaxf(M, m2);
+    if (mn == -INFINITY) return;
+    const float c1 = __expf(M - mn), c2 = __expf(m2 - mn);
+    l = l * c1 + l2 * c2;
+    acc.x = acc.x * c1 + a2.x * c2;
+    acc.y = acc.y * c1 + a2.y * c2;
+    acc.z = acc.z * c1 + a2.z * c2;
+    acc.w = acc.w * c1 + a2.w * c2;
+    M = mn;
+}
+
+__device__ __forceinline__ void merge_partial_rows(const float* __restrict__ part_m,
+                                                   const float* __restrict__ part_l,
+                                                   const float* __restrict__ part_acc, size_t row0,
+                                                   size_t stride, int count, uint16_t* __restrict__ out_row,
+                                                   float* __restrict__ lse_out) {
+    const int d4 = threadIdx.x / kMergeLanes, r = threadIdx.x % kMergeLanes;
+    float M = -INFINITY, l = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    constexpr int U = 8;
+    for (int s0 = r; s0 < count; s0 += U * kMergeLanes) {
+        float ms[U], ls[U];
+        float4 as[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = s0 + u * kMergeLanes;
+            ms[u] = -INFINITY;
+            ls[u] = 0.f;
+            as[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (s < count) {
+                const size_t row = row0 + (size_t)s * stride;
+                ms[u] = part_m[row];
+                ls[u] = part_l[row];
+                as[u] = *reinterpret_cast<const float4*>(part_acc + row * kD + 4 * d4);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) lse_fold(M, l, acc, ms[u], ls[u], as[u]);
+    }
+#pragma unroll
+    for (int o = 1; o < kMergeLanes; o <<= 1) {
+        const float M2 = __shfl_xor(M, o), l2 = __shfl_xor(l, o);
+        const float4 a2 = make_float4(__shfl_xor(acc.x, o), __shfl_xor(acc.y, o), __shfl_xor(acc.z, o),
+                                      __shfl_xor(acc.w, o));
+        lse_fold(M, l, acc, M2, l2, a2);
+    }
+    if (r == 0) {
+        const bool any = M != -INFINITY;
+        const float inv = any ? 1.f / l : 0.f;
+        uint2 packed;
+        packed.x = (uint32_t)f32_to_bf16(acc.x * inv) | ((uint32_t)f32_to_bf16(acc.y * inv) << 16);
+        packed.y = (uint32_t)f32_to_bf16(acc.z * inv) | ((uint32_t)f32_to_bf16(acc.w * inv) << 16);
+        *reinterpret_cast<uint2*>(out_row + 4 * d4) = packed;
+        if (lse_out && d4 == 0) *lse_out = any ? M + logf(l) : -INFINITY;
+    }
+}
+
 }  // namespace ffd
