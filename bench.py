@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed FFD steps only (for rocprofv3 runs)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="with --profile-only: then one plain device copy of this many MiB, a "
+                         "reference kernel of known traffic for calibrating HBM byte counters")
     return ap.parse_args()
 
 
@@ -110,6 +113,29 @@ def time_steps(fn, steps, warmup, flush, stream, stages=False):
     return ms, wall, st
 
 
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "ffd_4x128k_hbm_traffic.json")
+
+
+def measured_traffic(kernel, workload, delta):
+    """HBM bytes per launch of `kernel` from the committed counter record (FETCH_SIZE and
+    WRITE_SIZE, each scaled by the factor a plain copy of known size gives), or None when the
+    record is for another workload or the kernel sources changed since it was taken."""
+    import hashlib
+    if workload != 3 or delta != 5.0 or not os.path.exists(TRAFFIC_RECORD):
+        return None, "not measured for this workload"
+    rec = json.load(open(TRAFFIC_RECORD))
+    for path, digest in rec["source_sha256"].items():
+        with open(os.path.join(ROOT, path), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None, f"stale: {path} changed since the counters were taken"
+    k = rec["kernels"].get(kernel)
+    if k is None:
+        return None, "kernel not in the record"
+    return k["hbm_bytes_per_launch"], (f"rocprofv3 FETCH_SIZE x {rec['calibration']['fetch_factor']} + "
+                                       f"WRITE_SIZE x {rec['calibration']['write_factor']} per launch, "
+                                       f"{os.path.relpath(TRAFFIC_RECORD, ROOT)}")
+
+
 def cpu_baseline(case, delta, budget_s):
     """The oracle's decode step (given the quantized keys) on host cores, over a bounded sample of
     (sequence, KV head) pairs, scaled to the whole step."""
@@ -167,7 +193,9 @@ def main():
     S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, args.splits)
     ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev)
     codes, absmax, resid = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
-    flush_buf = torch.ones((args.flush_mib << 20) // 4, dtype=torch.int32, device=dev)
+    # float32: torch.sum keeps the dtype, so the flush is one read-only reduction (an int32 buffer
+    # would first be cast to an int64 temporary, i.e. a 2 GiB write before every step)
+    flush_buf = torch.ones((args.flush_mib << 20) // 4, dtype=torch.float32, device=dev)
 
     class _ReadFlush:
         """Evicts the caches by reading flush_buf (the reduction writes one scalar)."""
@@ -205,13 +233,21 @@ def main():
     nbytes = algorithmic_bytes(case, keep, S)
 
     ms, wall = time_steps(ffd_step, args.steps, args.warmup, flush, stream)
+    if args.profile_only:
+        if args.copy_mib > 0:
+            src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.int32, device=dev)
+            dst = torch.empty_like(src)
+            flush.zero_()
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+        print(json.dumps({"profile_only": True, "ffd_us_mean": float(ms.mean() * 1e3),
+                          "copy_mib": args.copy_mib}))
+        return
     # per-kernel durations from library-recorded events, in separate steps: the event markers
     # between kernels add a few microseconds of gap, so these steps are not the headline figure
     _, _, stage_ms = time_steps(lambda ev: ffd_step(events=ev), max(10, args.steps // 2), 3, flush,
                                 stream, stages=True)
-    if args.profile_only:
-        print(json.dumps({"profile_only": True, "ffd_us_mean": float(ms.mean() * 1e3)}))
-        return
     us = float(ms.mean() * 1e3)
     tbps = nbytes["total"] / (us * 1e-6) / 1e12
 
@@ -244,6 +280,7 @@ def main():
     dom = names[int(np.argmax(stage_us))]
     dom_us = float(stage_us[names.index(dom)])
     dom_gbps = stage_bytes[dom] / (dom_us * 1e-6) / 1e9
+    traffic, traffic_src = measured_traffic(dom, args.workload, args.delta)
 
     G = case.G
     valid_blocks = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel()
@@ -283,7 +320,8 @@ def main():
         "stages_gbps": {k: round(stage_bytes[k] / (float(u) * 1e-6) / 1e9, 1)
                         for k, u in zip(names, stage_us)},
         "roofline": {"bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
                      "kernel": dom, "kernel_us": round(dom_us, 2),
                      "algorithmic_bytes": int(stage_bytes[dom]),
                      "timing": "HIP events recorded by the library on the launch stream around "
