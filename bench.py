@@ -1,17 +1,20 @@
 """Benchmark of one FFD decode step on one MI355X, with the dense flash-decode baseline beside it.
 
-A step is one ffd_decode_attention call (pseudo-max, 2-bit scan, top-delta decision, refinement,
-online softmax . V, split merge) over one batch of synthetic inputs already resident in HBM.
-Every timed step is preceded by an untimed 1 GiB read of another buffer that evicts the 256 MB
-Infinity Cache and the L2 with clean lines, so the step streams from HBM as it would between the
-layers of a real decode. (A write-based flush would leave up to 256 MB of dirty lines whose
-write-back then competes with the measured step; a plain 134 MB stream measures ~25 us after a
-read flush and ~48 us after a write flush on MI355X.)
+A step is one ffd_decode_attention call (scan + top-delta decision, refinement + online
+softmax . V, split merge: three kernels) over one batch of synthetic inputs already resident in
+HBM. Every timed step is preceded by an untimed 1 GiB read of another buffer (a float32 sum) that
+evicts the 256 MB Infinity Cache and the L2 with clean lines, so the step streams from HBM as it
+would between the layers of a real decode. The dense baseline is timed the same way. The step is
+also captured once in a HIP graph and its replays timed (``graph_us``); on this stack a replay is
+slower than direct launches, so the headline uses direct launches unless ``--graph`` is given.
 
-Prints ONE JSON line. ``value`` is microseconds per decode step (lower is better); effective HBM
-bandwidth is the algorithmic bytes of the step (scan of every valid token's codes and absmax,
-residual + values of the tokens in blocks kept by any head of a KV group, queries, outputs and
-split partials) divided by the step time.
+Prints ONE JSON line. ``value`` is the mean microseconds per decode step (lower is better). Effective HBM bandwidth is the
+algorithmic bytes of the step (scan of every valid token's codes and absmax, residual + values of
+the tokens in blocks kept by any head of a KV group, queries, outputs and split partials) divided
+by the step time. ``roofline`` is the dominant kernel's algorithmic bandwidth from per-kernel HIP
+events (recorded by the library between its kernels, in separate eager steps), with its HBM
+traffic from the committed rocprofv3 counter record. ``stream_ceiling`` measures a plain device copy
+under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep.
 """
 from __future__ import annotations
 
@@ -37,8 +40,8 @@ METRIC = ("µs/decode step + effective HBM TB/s at 128K ctx; speedup vs dense fl
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = 128K x 4 sequences)")
     ap.add_argument("--delta", type=float, default=5.0)
     ap.add_argument("--splits", type=int, default=0)
@@ -46,6 +49,12 @@ def parse():
     ap.add_argument("--dense-steps", type=int, default=20)
     ap.add_argument("--sweep-deltas", default="3,7", help="extra deltas timed (10 steps each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="headline from HIP graph replays of the captured step (default: direct "
+                         "launches; graph replays are always reported as graph_us)")
+    ap.add_argument("--context-sweep", default="",
+                    help="comma-separated context lengths in K (e.g. 4,8,16,32,64,128,256): "
+                         "workload 2's layout at each length, FFD vs dense")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed FFD steps only (for rocprofv3 runs)")
@@ -88,7 +97,7 @@ def time_steps(fn, steps, warmup, flush, stream, stages=False):
     four per-stage events inside the step (on the same stream); returns their [steps, 3] durations."""
     import torch
     for _ in range(warmup):
-        flush.zero_()
+        flush.flush()
         fn() if not stages else fn(None)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
@@ -100,7 +109,7 @@ def time_steps(fn, steps, warmup, flush, stream, stages=False):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        flush.zero_()
+        flush.flush()
         starts[i].record(stream)
         fn() if not stages else fn(stage_evs[i])
         ends[i].record(stream)
@@ -169,6 +178,118 @@ def cpu_baseline(case, delta, budget_s):
                       f"float64 numpy, host affinity {len(os.sched_getaffinity(0))} CPUs"}
 
 
+class Runner:
+    """Device buffers of one case, its quantized cache, outputs and workspaces, and the timed
+    FFD / dense steps (eager or replayed from a captured HIP graph)."""
+
+    def __init__(self, case, splits, flush_mib):
+        import torch
+
+        from paper_2609_00097_amd import ffd
+        self.torch, self.ffd, self.case, self.splits = torch, ffd, case, splits
+        dev = self.dev = torch.device("cuda:0")
+        self.stream = torch.cuda.current_stream(dev)
+
+        def up(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+        self.q, self.k, self.v = up(case.q), up(case.k), up(case.v)
+        self.lens = torch.from_numpy(case.seq_lens.astype(np.int32)).to(dev)
+        self.S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, splits)
+        self.ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev)
+        self.dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev, dense=True)
+        self.qk = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
+        # float32: torch.sum keeps the dtype, so the flush is one read-only reduction (an int32
+        # buffer would first be cast to an int64 temporary, i.e. a 2 GiB write before every step)
+        self.flush_buf = torch.ones((flush_mib << 20) // 4, dtype=torch.float32, device=dev)
+        self.out = torch.empty((case.B, case.Hq, case.D), dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty((case.B, case.Hq), dtype=torch.float32, device=dev)
+        self.mask = torch.empty((case.B, case.Hq, case.Lcap // 64), dtype=torch.uint8, device=dev)
+        # the cache write (once per prefill; reported, not part of the step)
+        qs, qe = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        self.flush()
+        qs.record(self.stream)
+        ffd.quantize_keys(self.k, out=self.qk)
+        qe.record(self.stream)
+        torch.cuda.synchronize()
+        self.quant_ms = qs.elapsed_time(qe)
+
+    def flush(self):
+        self.torch.sum(self.flush_buf)
+
+    def ffd_step(self, delta, events=None, mask=None):
+        c = self.case
+        self.ffd.decode_attention(self.q, *self.qk, self.v, self.lens, delta=delta, n_sink=c.n_sink,
+                                  n_local=c.n_local, num_splits=self.splits, workspace=self.ws,
+                                  out=self.out, lse=self.lse, mask=mask, stage_events=events)
+
+    def dense_step(self):
+        self.ffd.dense_decode_attention(self.q, self.k, self.v, self.lens, num_splits=self.splits,
+                                        workspace=self.dws, out=self.out, lse=self.lse)
+
+    def mask_for(self, delta):
+        self.ffd_step(delta, mask=self.mask)
+        self.torch.cuda.synchronize()
+        return self.mask.cpu().numpy().astype(bool)
+
+    def graph(self, fn):
+        """Capture fn (which allocates nothing) in a HIP graph; returns its replay function."""
+        torch = self.torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        self._graphs = getattr(self, "_graphs", []) + [g]
+        return g.replay
+
+    def time(self, fn, steps, warmup, stages=False):
+        return time_steps(fn, steps, warmup, self, self.stream, stages=stages)
+
+
+def stream_ceiling(r, reps=10):
+    """Plain read (float32 sum) and plain copy of 512 MiB under the bench's flush protocol."""
+    torch = r.torch
+    n = (512 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=r.dev)
+    dst = torch.empty_like(src)
+    cp, _ = time_steps(lambda: dst.copy_(src), reps, 2, r, r.stream)
+    del src, dst
+    mb = (n * 4) / 1e6
+    return {"copy_tbps": round(2 * mb / (float(np.median(cp)) * 1e-3) / 1e6, 3),
+            "bytes": int(n * 4), "what": "torch copy_ of 512 MiB after a 1 GiB read flush, median of "
+                                         "10, HIP events; counts read + write bytes"}
+
+
+def context_sweep(lengths_k, splits, flush_mib, delta, steps, graph):
+    """FFD and dense step times at workload 2's layout for each context length."""
+    import ffd_inputs as I
+    out = {}
+    for lk in lengths_k:
+        case = I.context_case(lk * 1024)
+        r = Runner(case, splits, flush_mib)
+        keep = r.mask_for(delta)
+        nb = algorithmic_bytes(case, keep, r.S)
+        ffd_fn = r.graph(lambda: r.ffd_step(delta)) if graph else (lambda: r.ffd_step(delta))
+        dense_fn = r.graph(r.dense_step) if graph else r.dense_step
+        f_ms, _ = r.time(ffd_fn, steps, 5)
+        d_ms, _ = r.time(dense_fn, steps, 5)
+        f_us, d_us = float(f_ms.mean() * 1e3), float(d_ms.mean() * 1e3)
+        out[f"{lk}K"] = {"ffd_us": round(f_us, 2), "dense_us": round(d_us, 2),
+                         "speedup_vs_dense": round(d_us / f_us, 2),
+                         "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
+                         "dense_tbps": round(dense_bytes(case, r.S) / (d_us * 1e-6) / 1e12, 3),
+                         "keep_union_tokens": round(nb["gather_tokens"] / float(case.seq_lens.sum() * case.Hkv), 5)}
+        del r
+        import torch
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -176,100 +297,60 @@ def main():
               "(each (sequence, KV head) pair is independent; see the design notes)", file=sys.stderr)
         sys.exit(2)
 
-    import torch
+    import torch  # noqa: F401  (initialises the HIP runtime before the library is used)
 
     import ffd_inputs as I
-    from paper_2609_00097_amd import ffd
 
-    dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream(dev)
     case = I.workload(args.workload)
-
-    def up(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
-
-    q, k, v = up(case.q), up(case.k), up(case.v)
-    lens = torch.from_numpy(case.seq_lens.astype(np.int32)).to(dev)
-    S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, args.splits)
-    ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev)
-    codes, absmax, resid = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
-    # float32: torch.sum keeps the dtype, so the flush is one read-only reduction (an int32 buffer
-    # would first be cast to an int64 temporary, i.e. a 2 GiB write before every step)
-    flush_buf = torch.ones((args.flush_mib << 20) // 4, dtype=torch.float32, device=dev)
-
-    class _ReadFlush:
-        """Evicts the caches by reading flush_buf (the reduction writes one scalar)."""
-        def zero_(self):
-            torch.sum(flush_buf)
-    flush = _ReadFlush()
-
-    # cache write (once per prefill; reported, not part of the step)
-    qs, qe = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    flush.zero_()
-    qs.record(stream)
-    ffd.quantize_keys(k, out=(codes, absmax, resid))
-    qe.record(stream)
-    torch.cuda.synchronize()
-    quant_ms = qs.elapsed_time(qe)
-
-    out = torch.empty((case.B, case.Hq, case.D), dtype=torch.bfloat16, device=dev)
-    lse = torch.empty((case.B, case.Hq), dtype=torch.float32, device=dev)
-    mask = torch.empty((case.B, case.Hq, case.Lcap // 64), dtype=torch.uint8, device=dev)
-
-    def ffd_step(delta=args.delta, events=None):
-        ffd.decode_attention(q, codes, absmax, resid, v, lens, delta=delta, n_sink=case.n_sink,
-                             n_local=case.n_local, num_splits=args.splits, workspace=ws, out=out,
-                             lse=lse, stage_events=events)
+    r = Runner(case, args.splits, args.flush_mib)
+    S = r.S
 
     # the measured mask gives the algorithmic bytes (mask output off in the timed steps)
-    def mask_for(delta):
-        ffd.decode_attention(q, codes, absmax, resid, v, lens, delta=delta, n_sink=case.n_sink,
-                             n_local=case.n_local, num_splits=args.splits, workspace=ws, out=out,
-                             lse=lse, mask=mask)
-        torch.cuda.synchronize()
-        return mask.cpu().numpy().astype(bool)
-
-    keep = mask_for(args.delta)
+    keep = r.mask_for(args.delta)
     nbytes = algorithmic_bytes(case, keep, S)
 
-    ms, wall = time_steps(ffd_step, args.steps, args.warmup, flush, stream)
+    eager_ms, wall = r.time(lambda: r.ffd_step(args.delta), args.steps, args.warmup)
     if args.profile_only:
         if args.copy_mib > 0:
-            src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.int32, device=dev)
+            src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.int32, device=r.dev)
             dst = torch.empty_like(src)
-            flush.zero_()
+            r.flush()
             torch.cuda.synchronize()
             dst.copy_(src)
             torch.cuda.synchronize()
-        print(json.dumps({"profile_only": True, "ffd_us_mean": float(ms.mean() * 1e3),
+        print(json.dumps({"profile_only": True, "ffd_us_mean": float(eager_ms.mean() * 1e3),
                           "copy_mib": args.copy_mib}))
         return
-    # per-kernel durations from library-recorded events, in separate steps: the event markers
-    # between kernels add a few microseconds of gap, so these steps are not the headline figure
-    _, _, stage_ms = time_steps(lambda ev: ffd_step(events=ev), max(10, args.steps // 2), 3, flush,
-                                stream, stages=True)
+    graph_ms, graph_wall = r.time(r.graph(lambda: r.ffd_step(args.delta)), args.steps, args.warmup)
+    ms = graph_ms if args.graph else eager_ms
+    wall = graph_wall if args.graph else wall
     us = float(ms.mean() * 1e3)
+    eager_us = float(eager_ms.mean() * 1e3)
+    graph_us = float(graph_ms.mean() * 1e3)
     tbps = nbytes["total"] / (us * 1e-6) / 1e12
 
-    # dense flash-decode baseline, same protocol
-    dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, args.splits, dev, dense=True)
+    # per-kernel durations from library-recorded events, in separate eager steps: the event
+    # markers between kernels add a few microseconds of gap, so these steps are not the headline
+    _, _, stage_ms = r.time(lambda ev: r.ffd_step(args.delta, events=ev), max(10, args.steps // 2), 3,
+                            stages=True)
 
-    def dense_step():
-        ffd.dense_decode_attention(q, k, v, lens, num_splits=args.splits, workspace=dws, out=out,
-                                   lse=lse)
-    dms, _ = time_steps(dense_step, args.dense_steps, 3, flush, stream)
+    # dense flash-decode baseline, same protocol
+    dms, _ = r.time(r.graph(r.dense_step) if args.graph else r.dense_step, args.dense_steps, 3)
     dense_us = float(dms.mean() * 1e3)
     dbytes = dense_bytes(case, S)
 
     sweep = {}
     for d in [float(x) for x in args.sweep_deltas.split(",") if x.strip()]:
-        kd = mask_for(d)
+        kd = r.mask_for(d)
         bd = algorithmic_bytes(case, kd, S)
-        sms, _ = time_steps(lambda: ffd_step(d), 10, 2, flush, stream)
+        fn = r.graph(lambda: r.ffd_step(d)) if args.graph else (lambda: r.ffd_step(d))
+        sms, _ = r.time(fn, 20, 3)
         su = float(sms.mean() * 1e3)
         sweep[str(d)] = {"us": round(su, 2), "tbps": round(bd["total"] / (su * 1e-6) / 1e12, 3),
                          "keep_head_blocks": round(float(kd.mean()), 5),
                          "speedup_vs_dense": round(dense_us / su, 2)}
+
+    ceiling = stream_ceiling(r)
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
     stage_us = stage_ms.mean(axis=0) * 1e3
@@ -282,7 +363,6 @@ def main():
     dom_gbps = stage_bytes[dom] / (dom_us * 1e-6) / 1e9
     traffic, traffic_src = measured_traffic(dom, args.workload, args.delta)
 
-    G = case.G
     valid_blocks = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel()
                                    for b in range(case.B)])
     union_frac = nbytes["gather_tokens"] / float(np.sum(case.seq_lens) * case.Hkv)
@@ -303,18 +383,22 @@ def main():
                    "q_heads": case.Hq, "kv_heads": case.Hkv, "head_dim": case.D, "kv_block": 64,
                    "delta": args.delta, "n_sink": case.n_sink, "n_local": case.n_local,
                    "num_splits": S, "io": "q/v/out bf16, k as 2-bit codes + int8 residual",
+                   "launch": "hip graph replay" if args.graph else "direct (stream-ordered) launches",
                    "cache_flush_between_steps_mib": args.flush_mib, "cache_flush": "read"},
         "effective_tbps": round(tbps, 3),
         "hbm_peak_frac": round(tbps * 1e3 / HBM_PEAK_GBPS, 4),
         "bytes_per_step": nbytes,
         "us_p10_p50_p90": [round(float(np.percentile(ms, p)) * 1e3, 2) for p in (10, 50, 90)],
+        "eager_us": round(eager_us, 2),
+        "graph_us": round(graph_us, 2),
         "keep_head_blocks": round(float(valid_blocks.mean()), 5),
         "keep_union_tokens": round(union_frac, 5),
         "dense_us": round(dense_us, 2),
         "dense_tbps": round(dbytes / (dense_us * 1e-6) / 1e12, 3),
         "speedup_vs_dense": round(dense_us / us, 2),
         "delta_sweep": sweep,
-        "quantize_cache_us": round(quant_ms * 1e3, 1),
+        "stream_ceiling": ceiling,
+        "quantize_cache_us": round(r.quant_ms * 1e3, 1),
         "wall_s_timed_region": round(wall, 3),
         "stages_us": {k: round(float(u), 2) for k, u in zip(names, stage_us)},
         "stages_gbps": {k: round(stage_bytes[k] / (float(u) * 1e-6) / 1e9, 1)
@@ -325,8 +409,13 @@ def main():
                      "kernel": dom, "kernel_us": round(dom_us, 2),
                      "algorithmic_bytes": int(stage_bytes[dom]),
                      "timing": "HIP events recorded by the library on the launch stream around "
-                               "each kernel, mean over the timed steps"},
+                               "each kernel, mean over separate eager steps"},
     }
+    if args.context_sweep:
+        del r
+        torch.cuda.empty_cache()
+        line["context_sweep"] = context_sweep([int(x) for x in args.context_sweep.split(",") if x.strip()],
+                                              args.splits, args.flush_mib, args.delta, 30, args.graph)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(case, args.delta, args.cpu_seconds)
     print(json.dumps(line))

@@ -227,6 +227,19 @@ def workload(n: int, seed: int | None = None) -> Case:
     raise KeyError(n)
 
 
+def context_case(L: int, seed: int | None = None) -> Case:
+    """Workload 2's layout (B = 1, 32 q / 8 KV heads, 2% heavy blocks + sink) at context length L,
+    for the context-length sweep (4K .. 256K)."""
+    if L <= 0 or L % BLOCK:
+        raise ValueError("L must be a positive multiple of 64")
+    seed = 2000 + L // 1024 if seed is None else seed
+    return generate(name=f"ctx-sweep-{L // 1024}k-b1-32q8kv", seed=seed, B=1, Hq=32, Hkv=8, Lcap=L,
+                    seq_lens=[L],
+                    heavy_fn=lambda rng, b, h, L: _random_blocks(rng, L, BLOCK, DEFAULT_N_LOCAL,
+                                                                  round(0.02 * (L // BLOCK))),
+                    deltas=(5.0,))
+
+
 def small_case(*, seed, B=1, Hq=8, Hkv=2, seq_lens=(1000,), Lcap=None, heavy_frac=0.03,
                sink=True, recent_tokens=0, n_sink=DEFAULT_N_SINK, n_local=DEFAULT_N_LOCAL,
                deltas=(5.0,), name="small") -> Case:
