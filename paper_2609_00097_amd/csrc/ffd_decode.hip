@@ -648,8 +648,6 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                        a.part_l, a.part_acc);
 }
 
-
-
 template __global__ void ffd_scan_kernel<1>(ScanArgs);
 template __global__ void ffd_scan_kernel<2>(ScanArgs);
 template __global__ void ffd_refine_kernel<1>(RefineArgs);

@@ -221,8 +221,8 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
 // output row and lse (Sec. 2, flash-decoding): M* = max m_i, l* = sum e^{m_i - M*} l_i,
 // out = sum e^{m_i - M*} acc_i / l*, lse = M* + ln l*. Rows with m = -inf are skipped; no row
 // gives out = 0, lse = -inf. Run by all 256 threads of a workgroup: thread (d4, r) folds rows
-// i = r (mod 8) of dims 4*d4 .. 4*d4 + 3 with 8 float4 loads in flight, then the 8 threads of a
-// d4 combine with shuffles.
+// i = r (mod 8) of dims 4*d4 .. 4*d4 + 3, U rows at a time with the next U rows' loads already in
+// flight (a head can have hundreds of partials), then the 8 threads of a d4 combine with shuffles.
 constexpr int kMergeLanes = 8;
 
 __device__ __forceinline__ void lse_fold(float& M, float& l, float4& acc, float m2, float l2, float4 a2) {
@@ -237,6 +237,30 @@ __device__ __forceinline__ void lse_fold(float& M, float& l, float4& acc, float 
     M = mn;
 }
 
+template <int U>
+struct MergeBatch {
+    float m[U], l[U];
+    float4 a[U];
+};
+
+// Rows s0 + u * kMergeLanes (u < U) of the head, or empty rows (m = -inf) past count. The row
+// index is clamped so the loads are unconditional.
+template <int U>
+__device__ __forceinline__ void load_merge_batch(MergeBatch<U>& bt, const float* __restrict__ part_m,
+                                                 const float* __restrict__ part_l,
+                                                 const float* __restrict__ part_acc, size_t row0,
+                                                 size_t stride, int count, int s0, int d4) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int s = s0 + u * kMergeLanes;
+        const size_t row = row0 + (size_t)min(s, count - 1) * stride;
+        bt.m[u] = part_m[row];
+        bt.l[u] = part_l[row];
+        bt.a[u] = *reinterpret_cast<const float4*>(part_acc + row * kD + 4 * d4);
+        if (s >= count) bt.m[u] = -INFINITY;
+    }
+}
+
 __device__ __forceinline__ void merge_partial_rows(const float* __restrict__ part_m,
                                                    const float* __restrict__ part_l,
                                                    const float* __restrict__ part_acc, size_t row0,
@@ -246,24 +270,16 @@ __device__ __forceinline__ void merge_partial_rows(const float* __restrict__ par
     float M = -INFINITY, l = 0.f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     constexpr int U = 8;
-    for (int s0 = r; s0 < count; s0 += U * kMergeLanes) {
-        float ms[U], ls[U];
-        float4 as[U];
+    constexpr int kStep = U * kMergeLanes;
+    if (count > 0) {
+        MergeBatch<U> cur, nxt;
+        load_merge_batch<U>(cur, part_m, part_l, part_acc, row0, stride, count, r, d4);
+        for (int s0 = r; s0 < count; s0 += kStep) {
+            load_merge_batch<U>(nxt, part_m, part_l, part_acc, row0, stride, count, s0 + kStep, d4);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int s = s0 + u * kMergeLanes;
-            ms[u] = -INFINITY;
-            ls[u] = 0.f;
-            as[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (s < count) {
-                const size_t row = row0 + (size_t)s * stride;
-                ms[u] = part_m[row];
-                ls[u] = part_l[row];
-                as[u] = *reinterpret_cast<const float4*>(part_acc + row * kD + 4 * d4);
-            }
+            for (int u = 0; u < U; ++u) lse_fold(M, l, acc, cur.m[u], cur.l[u], cur.a[u]);
+            cur = nxt;
         }
-#pragma unroll
-        for (int u = 0; u < U; ++u) lse_fold(M, l, acc, ms[u], ls[u], as[u]);
     }
 #pragma unroll
     for (int o = 1; o < kMergeLanes; o <<= 1) {
