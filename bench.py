@@ -251,6 +251,41 @@ class Runner:
         return time_steps(fn, steps, warmup, self, self.stream, stages=stages)
 
 
+def decode_loop(r, delta, steps, warmup):
+    """Decode-loop step: append one token per sequence (ffd_append_kv) then attend. The lengths
+    start 256 tokens below capacity so every timed step has room; each step grows the cache by one
+    token. Times the append alone, append + attention with direct launches, and the same two calls
+    captured once in a HIP graph and replayed (no re-capture as the cache grows)."""
+    torch, ffd, c = r.torch, r.ffd, r.case
+    room = warmup + steps + 4
+    lens0 = torch.clamp(r.lens - 256, min=0)
+    lens = lens0.clone()
+    gen = torch.Generator(device=r.dev).manual_seed(1)
+    k_new = torch.randn((c.B, c.Hkv, c.D), device=r.dev, generator=gen).to(torch.bfloat16)
+    v_new = torch.randn((c.B, c.Hkv, c.D), device=r.dev, generator=gen).to(torch.bfloat16)
+
+    def append():
+        ffd.append_kv(k_new, v_new, r.qk, lens, k_cache=r.k, v_cache=r.v)
+
+    def step():
+        append()
+        ffd.decode_attention(r.q, *r.qk, r.v, lens, delta=delta, n_sink=c.n_sink, n_local=c.n_local,
+                             num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse)
+    assert 3 * room <= 256, "not enough room for the appends"
+    lens.copy_(lens0)
+    a_ms, _ = r.time(append, steps, warmup)
+    lens.copy_(lens0)
+    s_ms, _ = r.time(step, steps, warmup)
+    lens.copy_(lens0)
+    g_ms, _ = r.time(r.graph(step), steps, warmup)
+    return {"append_us": round(float(a_ms.mean() * 1e3), 2),
+            "append_plus_attention_us": round(float(s_ms.mean() * 1e3), 2),
+            "graph_append_plus_attention_us": round(float(g_ms.mean() * 1e3), 2),
+            "what": "one token appended per sequence (bf16 K/V rows + quantized key, length advanced "
+                    "on the device) then the decode attention, starting 256 tokens below capacity; "
+                    "the graph is captured once and replayed while the cache grows"}
+
+
 def stream_ceiling(r, reps=10):
     """Plain read (float32 sum) and plain copy of 512 MiB under the bench's flush protocol."""
     torch = r.torch
@@ -351,6 +386,7 @@ def main():
                          "speedup_vs_dense": round(dense_us / su, 2)}
 
     ceiling = stream_ceiling(r)
+    loop = decode_loop(r, args.delta, min(args.steps, 60), 10)      # writes the caches: run last
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
     stage_us = stage_ms.mean(axis=0) * 1e3
@@ -398,6 +434,7 @@ def main():
         "speedup_vs_dense": round(dense_us / us, 2),
         "delta_sweep": sweep,
         "stream_ceiling": ceiling,
+        "decode_loop": loop,
         "quantize_cache_us": round(r.quant_ms * 1e3, 1),
         "wall_s_timed_region": round(wall, 3),
         "stages_us": {k: round(float(u), 2) for k, u in zip(names, stage_us)},

@@ -5,6 +5,8 @@
  *
  *   ffd_quantize_keys           split each key into a 2-bit thumbnail and an 8-bit residual
  *                               (Sec. 3.1; App. A formulation; Fig. 2 "K quantization").
+ *   ffd_append_kv               append one decode token per sequence to the bf16 and quantized
+ *                               caches at its device-side length, and advance the length.
  *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), 2-bit scan and
  *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement that reuses
  *                               the scan dot products (Eq. 4), online-softmax attention over the kept
@@ -75,6 +77,25 @@ typedef enum {
  */
 int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resid,
                       int B, int Hkv, int Lcap, int D, int t_begin, int t_end, hipStream_t stream);
+
+/*
+ * Decode-step append, the cache update before attention in each step of a decode loop (the cache
+ * grows by one token per step; the key is split as by ffd_quantize_keys, Sec. 3.1 and App. A). For
+ * every sequence b with L = seq_lens[b] < Lcap: k_new[b] and v_new[b] are written at position L of
+ * the bf16 caches (each cache pointer may be NULL to skip it), k_new[b] is quantized into codes,
+ * absmax and residual at position L, and seq_lens[b] becomes L + 1. A sequence with L >= Lcap (or
+ * L < 0) is left unchanged. Everything happens on the device, so the call can be captured in a HIP
+ * graph together with ffd_decode_attention and the graph replayed as the cache grows (the kernels
+ * read the lengths from seq_lens and size their grids from Lcap).
+ *
+ *   k_new, v_new   bf16 [B, Hkv, D]          the new token's key and value (read)
+ *   k_cache, v_cache  bf16 [B, Hkv, Lcap, D]  or NULL
+ *   k_codes, k_absmax, k_resid                quantized key layouts above
+ *   seq_lens       int32 [B] (device, read and written)
+ */
+int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, void* k_codes,
+                  void* k_absmax, void* k_resid, int32_t* seq_lens, int B, int Hkv, int Lcap, int D,
+                  hipStream_t stream);
 
 /*
  * FFD decode attention (Alg. 1 with Eq. 1-4), one query per head.

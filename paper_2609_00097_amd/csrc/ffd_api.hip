@@ -176,6 +176,25 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
     return launch_status();
 }
 
+int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, void* k_codes,
+                  void* k_absmax, void* k_resid, int32_t* seq_lens, int B, int Hkv, int Lcap, int D,
+                  hipStream_t stream) {
+    int st = check_shapes(B, Hkv, Hkv, Lcap, D);
+    if (st != FFD_OK) return st;
+    if (B == 0) return FFD_OK;
+    if (!k_new || !v_new || !k_codes || !k_absmax || !k_resid || !seq_lens) return FFD_ERR_INVALID_ARGUMENT;
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_codes) || !aligned16(k_absmax) ||
+        !aligned16(k_resid) || (k_cache && !aligned16(k_cache)) || (v_cache && !aligned16(v_cache)) ||
+        (reinterpret_cast<uintptr_t>(seq_lens) & 3u))
+        return FFD_ERR_INVALID_ARGUMENT;
+    AppendArgs a{static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                 static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
+                 static_cast<uint32_t*>(k_codes), static_cast<uint16_t*>(k_absmax),
+                 static_cast<int8_t*>(k_resid), seq_lens, Hkv, Lcap};
+    hipLaunchKernelGGL(append_kv_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, a);
+    return launch_status();
+}
+
 int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
                                 const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
                                 int Hkv, int Lcap, int D, int block_size, float delta, int n_sink,

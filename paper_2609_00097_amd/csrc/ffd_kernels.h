@@ -64,10 +64,23 @@ struct QuantArgs {
     int Hkv, Lcap, t_begin, t_end;
 };
 
+struct AppendArgs {
+    const uint16_t* k_new;      // bf16 [B, Hkv, 128]
+    const uint16_t* v_new;      // bf16 [B, Hkv, 128]
+    uint16_t* k_cache;          // bf16 [B, Hkv, Lcap, 128] or null
+    uint16_t* v_cache;          // bf16 [B, Hkv, Lcap, 128] or null
+    uint32_t* codes;
+    uint16_t* absmax;
+    int8_t* resid;
+    int32_t* seq_lens;          // [B], read and advanced
+    int Hkv, Lcap;
+};
+
 template <int NT> __global__ void ffd_scan_kernel(ScanArgs a);
 template <int NT> __global__ void ffd_refine_kernel(RefineArgs a);
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
 __global__ void quantize_keys_kernel(QuantArgs a);
+__global__ void append_kv_kernel(AppendArgs a);
 __global__ void lse_merge_kernel(const float* part_m, const float* part_l, const float* part_acc, int S,
                                  const int2* table, int G, uint16_t* out, float* lse);
 

@@ -21,7 +21,7 @@ MAX_SPLITS = 1024
 STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
           3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
 
-EXPORTS = ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
            "ffd_dense_decode_attention",
            "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
@@ -54,6 +54,7 @@ def lib() -> ctypes.CDLL:
     except OSError as e:
         raise FfdLibraryError(f"cannot load {LIB_PATH}: {e}") from e
     so.ffd_quantize_keys.argtypes = [P, P, P, P, I, I, I, I, I, I, P]
+    so.ffd_append_kv.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, P]
     so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, I, I, F,
                                         P, P, P, P, SZ, P]
     so.ffd_decode_attention_events.argtypes = so.ffd_decode_attention.argtypes + [P]
@@ -64,7 +65,7 @@ def lib() -> ctypes.CDLL:
         getattr(so, name).restype = SZ
     so.ffd_status_string.argtypes = [I]
     so.ffd_status_string.restype = ctypes.c_char_p
-    for name in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+    for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
                  "ffd_dense_decode_attention", "ffd_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
@@ -141,6 +142,27 @@ def quantize_keys(k: torch.Tensor, t_begin: int = 0, t_end: int | None = None, o
         _ptr(k), _ptr(codes), _ptr(absmax), _ptr(resid), B, Hkv, Lcap, D, t_begin, t_end,
         _stream(k.device)))
     return codes, absmax, resid
+
+
+def append_kv(k_new, v_new, quantized, seq_lens, *, k_cache=None, v_cache=None):
+    """Append one token per sequence at position ``seq_lens[b]`` (device-side) to the quantized key
+    cache ``(codes, absmax, resid)`` and, when given, the bf16 caches ``[B, Hkv, Lcap, 128]``; then
+    ``seq_lens[b] += 1`` for every sequence below capacity. ``k_new``/``v_new``: bf16 ``[B, Hkv, 128]``."""
+    codes, absmax, resid = quantized
+    B, Hkv, D = k_new.shape
+    Lcap = codes.shape[2] * 64
+    _need(k_new, "k_new", torch.bfloat16)
+    _need(v_new, "v_new", torch.bfloat16, (B, Hkv, D))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
+                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
+        _need(t, nm, dt, sh)
+    for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        if t is not None:
+            _need(t, nm, torch.bfloat16, (B, Hkv, Lcap, D))
+    _check("ffd_append_kv", lib().ffd_append_kv(
+        _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(codes), _ptr(absmax), _ptr(resid),
+        _ptr(seq_lens), B, Hkv, Lcap, D, _stream(k_new.device)))
 
 
 def _attn_outputs(q, B, Hq, Lcap, want_lse, want_mask, out, lse, mask):

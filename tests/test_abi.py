@@ -25,7 +25,7 @@ def so():
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("ffd_quantize_keys", "ffd_decode_attention", "ffd_decode_attention_events",
+    for n in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
               "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes",
               "ffd_status_string"):
         assert n in names
@@ -91,6 +91,17 @@ def test_misaligned_and_small_workspace(so):
     need = so.ffd_dense_workspace_bytes(1, 32, 8, 4096, 128, 0)
     assert so.ffd_dense_decode_attention(fake, fake, fake, fake, 1, 32, 8, 4096, 128, 0, 0.0, fake, None,
                                          fake, need - 1, None) == 3
+
+
+def test_append_argument_checks(so):
+    fake = 0x1000
+    # null pointers, misalignment, bad shapes: rejected before any launch
+    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 1, 8, 4096, 128, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake + 2, 1, 8, 4096, 128, None) == 1
+    assert so.ffd_append_kv(fake, fake + 8, None, None, fake, fake, fake, fake, 1, 8, 4096, 128, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 100, 128, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 4096, 96, None) == 2
+    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 0, 8, 4096, 128, None) == 0
 
 
 def test_quantize_range_checks(so):
