@@ -18,6 +18,9 @@ Readings of the paper taken where it is silent or ambiguous (each is listed in t
 * Residual (Sec. 3.1 "8-bit residual"): an int8 ``r`` on the shared step ``s / 254`` so that
   ``k^quant + k^res = (s)(level + r/254) = M n / 381`` with ``n = rint(381 k / M)`` (ties to even)
   and ``r = n - 254 c + 381`` in ``[-127, 127]``.
+* Wider thumbnails (App. C, the 4+8 and 8+8 depths): the same mid-rise scheme with ``2^b`` levels
+  ``c - Lv``, ``Lv = (2^b - 1)/2``, ``s = M / Lv``, and the same 8-bit residual on ``s / 254``, so
+  ``n = rint(254 Lv k / M)`` and ``r = n - 254 c + 254 Lv``. ``b = 2`` is the formulation above.
 * All scores (scan, pseudo-max, block score, refined logits) carry the ``1/sqrt(d)`` of Eq. 1.
 * The pseudo-max (Alg. 1; Eq. 3) is taken over thumbnail scores of the first ``n_sink`` tokens and
   the last ``n_local`` tokens of the sequence.
@@ -33,6 +36,22 @@ import numpy as np
 CODEBOOK = np.array([-1.5, -0.5, 0.5, 1.5], dtype=np.float64)
 RESID_STEPS = 254          # residual step is s / 254 (Sec. 3.1 8-bit residual reading)
 FULL_LEVELS = 381          # 1.5 * 254: k^quant + k^res = M * n / 381
+THUMB_BITS = (2, 4, 8)     # thumbnail depths of App. C (2+8, 4+8, 8+8)
+
+
+def top_level(bits: int = 2) -> float:
+    """``Lv = (2^b - 1) / 2``: the outer level of the b-bit mid-rise codebook (1.5 for App. A)."""
+    return (2 ** bits - 1) / 2.0
+
+
+def codebook(bits: int = 2) -> np.ndarray:
+    """The ``2^b`` levels ``c - Lv`` for ``c = 0 .. 2^b - 1`` (App. A's codebook when ``b = 2``)."""
+    return np.arange(2 ** bits, dtype=np.float64) - top_level(bits)
+
+
+def full_levels(bits: int = 2) -> int:
+    """``254 Lv``: thumbnail plus residual is ``M n / full_levels`` (381 for 2+8, 32385 for 8+8)."""
+    return RESID_STEPS * (2 ** bits - 1) // 2
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -53,39 +72,54 @@ def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
 # Q1/Q2. Key decomposition k -> {k^quant, k^res} (Sec. 3.1; App. A formulation).
 # ------------------------------------------------------------------------------------------------
 
-def quantize_keys(K: np.ndarray):
-    """Thumbnail codes, absmax and residual of every key vector (App. A; Sec. 3.1).
+def quantize_keys(K: np.ndarray, bits: int = 2):
+    """Thumbnail codes, absmax and residual of every key vector (App. A; Sec. 3.1; App. C depths).
 
-    ``K``: float64 ``[..., d]`` of bf16-exact values. Returns ``codes`` (int64 in 0..3),
+    ``K``: float64 ``[..., d]`` of bf16-exact values. Returns ``codes`` (int64 in ``0 .. 2^b - 1``),
     ``M`` (float64 ``[...]``, the per-vector absmax) and ``resid`` (int64 in -127..127).
 
-    The nearest-level rule of App. A is applied with exact comparisons: ``x/s`` against the bin
-    edges -1, 0, +1 is ``3k`` against ``-2M, 0, 2M``; a tie goes to the upper level.
+    Nearest level: with ``x/s = Lv k / M`` the edges between consecutive levels ``c - 1 - Lv`` and
+    ``c - Lv`` are the integers ``c - 2^(b-1)``, so the nearest level has ``c = floor(x/s) + 2^(b-1)``
+    and a value on an edge goes to the upper level. ``floor(x/s) = floor((2^b - 1) k / (2M))`` is
+    taken in float64 and then settled by exact comparisons (``(2^b - 1) k`` and ``i * 2M`` are
+    products of two 8-bit significands, exact in float64). For ``b = 2`` this is ``3k`` against
+    ``-2M, 0, 2M``.
+
+    Residual: ``n = rint(254 Lv k / M)`` (round half to even). ``254 Lv k`` is exact in float64; a
+    quotient ``Q`` that is not a tie lies at least ``2^-24 Q`` from every half-integer (its distance
+    is a multiple of half the unit of ``k`` over ``M``, and ``254 Lv < 2^15``), while the division
+    moves it by at most ``2^-53 Q``, so the rounding is the exact one.
     """
     K = np.asarray(K, dtype=np.float64)
     M = np.max(np.abs(K), axis=-1)
     Mx = M[..., None]
-    codes = np.where(3.0 * K >= 2.0 * Mx, 3,
-                     np.where(K >= 0.0, 2,
-                              np.where(3.0 * K >= -2.0 * Mx, 1, 0))).astype(np.int64)
+    u = (2 ** bits - 1) * K
+    D = 2.0 * Mx
     zero = Mx == 0.0
-    codes = np.where(zero, 2, codes)
     with np.errstate(divide="ignore", invalid="ignore"):
-        n = np.rint(FULL_LEVELS * K / Mx)          # round half to even
+        i = np.floor(u / D)
+    i = np.where(zero, 0.0, i)
+    i = np.where((i + 1.0) * D <= u, i + 1.0, i)
+    i = np.where(i * D > u, i - 1.0, i)
+    codes = np.clip(i + 2 ** (bits - 1), 0, 2 ** bits - 1).astype(np.int64)
+    codes = np.where(zero, 2 ** (bits - 1), codes)
+    N = full_levels(bits)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        n = np.rint(N * K / Mx)                    # round half to even
     n = np.where(zero, 0.0, n).astype(np.int64)
-    resid = np.where(zero, 0, n - RESID_STEPS * codes + FULL_LEVELS).astype(np.int64)
+    resid = np.where(zero, 0, n - RESID_STEPS * codes + N).astype(np.int64)
     return codes, M, resid
 
 
-def thumbnail(codes: np.ndarray, M: np.ndarray) -> np.ndarray:
-    """Dequantized thumbnail ``k^quant = x_q * s`` with ``s = M / 1.5`` (App. A reconstruction)."""
-    s = np.asarray(M, dtype=np.float64)[..., None] / 1.5
-    return CODEBOOK[codes] * s
+def thumbnail(codes: np.ndarray, M: np.ndarray, bits: int = 2) -> np.ndarray:
+    """Dequantized thumbnail ``k^quant = (c - Lv) s`` with ``s = M / Lv`` (App. A reconstruction)."""
+    s = np.asarray(M, dtype=np.float64)[..., None] / top_level(bits)
+    return codebook(bits)[codes] * s
 
 
-def residual_part(resid: np.ndarray, M: np.ndarray) -> np.ndarray:
-    """The residual's contribution ``k^res = s * r / 254`` (Sec. 3.1 reading; Eq. 4's second term)."""
-    s = np.asarray(M, dtype=np.float64)[..., None] / 1.5
+def residual_part(resid: np.ndarray, M: np.ndarray, bits: int = 2) -> np.ndarray:
+    """The residual's contribution ``k^res = s r / 254`` (Sec. 3.1 reading; Eq. 4's second term)."""
+    s = np.asarray(M, dtype=np.float64)[..., None] / top_level(bits)
     return s * (np.asarray(resid, dtype=np.float64) / RESID_STEPS)
 
 
@@ -93,9 +127,10 @@ def residual_part(resid: np.ndarray, M: np.ndarray) -> np.ndarray:
 # S1. Thumbnail scan (Alg. 1 top-delta loop; Sec. 3.3 step 2), scaled by 1/sqrt(d) (Eq. 1).
 # ------------------------------------------------------------------------------------------------
 
-def scan_scores(q: np.ndarray, codes: np.ndarray, M: np.ndarray, alpha: float) -> np.ndarray:
+def scan_scores(q: np.ndarray, codes: np.ndarray, M: np.ndarray, alpha: float,
+                bits: int = 2) -> np.ndarray:
     """``s_hat[h, t] = alpha * q_h . k^quant_t`` for every head of the group and every token."""
-    return alpha * (np.asarray(q, dtype=np.float64) @ thumbnail(codes, M).T)
+    return alpha * (np.asarray(q, dtype=np.float64) @ thumbnail(codes, M, bits).T)
 
 
 # ------------------------------------------------------------------------------------------------
@@ -139,10 +174,10 @@ def select_blocks(sigma: np.ndarray, m_tilde: np.ndarray, delta: float) -> np.nd
 # S4. Refinement with scan reuse (Alg. 1 refinement; Sec. 3.3 Eq. 4).
 # ------------------------------------------------------------------------------------------------
 
-def refined_logits(q, codes, M, resid, alpha):
+def refined_logits(q, codes, M, resid, alpha, bits=2):
     """``s_final = (q . k^quant + q . k^res) / sqrt(d)``: the scan term plus the residual term."""
     q = np.asarray(q, dtype=np.float64)
-    return alpha * (q @ thumbnail(codes, M).T + q @ residual_part(resid, M).T)
+    return alpha * (q @ thumbnail(codes, M, bits).T + q @ residual_part(resid, M, bits).T)
 
 
 # ------------------------------------------------------------------------------------------------
@@ -210,28 +245,29 @@ def lse_merge(states):
 # The whole decode step for one (sequence, KV head) group, and for a batch.
 # ------------------------------------------------------------------------------------------------
 
-def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None):
+def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None, bits=2):
     """FFD decode for the ``G`` query heads ``q [G, d]`` sharing keys ``K [Lcap, d]``, values ``V``.
 
     Follows Alg. 1 in order: quantize, pseudo-max, top-delta selection, refinement, softmax . V.
     When ``keep`` (bool ``[G, nblk]``) is given, attention runs on that mask instead of the
-    oracle's own selection (used to compare outputs given the GPU's mask).
+    oracle's own selection (used to compare outputs given the GPU's mask). ``bits`` is the
+    thumbnail depth (App. C).
     """
-    codes, M, resid = quantize_keys(K[:L])
+    codes, M, resid = quantize_keys(K[:L], bits)
     return decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=n_sink,
-                                  n_local=n_local, block=block, alpha=alpha, keep=keep)
+                                  n_local=n_local, block=block, alpha=alpha, keep=keep, bits=bits)
 
 
 def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, block, alpha,
-                           keep=None):
+                           keep=None, bits=2):
     """The decode step of :func:`decode_group` given the already quantized keys (Alg. 1 from the
     pseudo-max on; the quantization happens when the cache is written, Fig. 2)."""
-    s_hat = scan_scores(q, codes, M, alpha)
+    s_hat = scan_scores(q, codes, M, alpha, bits)
     m_tilde = pseudo_max(s_hat, L, n_sink, n_local)
     sigma = block_scores(s_hat, L, block)
     own_keep = select_blocks(sigma, m_tilde, delta)
     use = own_keep if keep is None else np.asarray(keep, dtype=bool)[:, :sigma.shape[1]]
-    z_all = refined_logits(q, codes, M, resid, alpha)
+    z_all = refined_logits(q, codes, M, resid, alpha, bits)
     outs, lses = [], []
     for h in range(q.shape[0]):
         tok = token_mask_from_blocks(use[h], L, block)
@@ -243,12 +279,13 @@ def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, 
 
 
 def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, block=64,
-                 softmax_scale=None, keep=None, heads=None):
+                 softmax_scale=None, keep=None, heads=None, bits=2):
     """FFD decode for a batch. Inputs are bf16 bit patterns ``q [B,Hq,d]``, ``k, v [B,Hkv,Lcap,d]``.
 
     Returns float64 ``out [B,Hq,d]``, ``lse [B,Hq]``, the per-head block mask ``keep [B,Hq,nblk]``
     (blocks at or beyond a sequence's end are False), ``sigma`` and ``m_tilde``.
-    ``heads`` optionally restricts work to a list of ``(b, kvh)`` pairs (others left as NaN).
+    ``heads`` optionally restricts work to a list of ``(b, kvh)`` pairs (others left as NaN);
+    ``bits`` is the thumbnail depth (App. C).
     """
     B, Hq, d = q_bits.shape
     Hkv, Lcap = k_bits.shape[1], k_bits.shape[2]
@@ -274,7 +311,7 @@ def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, bl
         V = bf16_to_f64(v_bits[b, h, :L])
         kb = None if keep is None else np.asarray(keep[b, sl], dtype=bool)
         r = decode_group(q, K, V, L, delta=delta, n_sink=n_sink, n_local=n_local, block=block,
-                         alpha=alpha, keep=kb)
+                         alpha=alpha, keep=kb, bits=bits)
         nb = r["sigma"].shape[1]
         out[b, sl] = r["out"]
         lse[b, sl] = r["lse"]
@@ -314,57 +351,74 @@ def near_threshold(sigma, m_tilde, delta, band=1e-3):
 # Storage layouts of the quantized copy (this implementation's format; the paper fixes none).
 # They are written out independently of the HIP code, from the format's definition:
 #
-#  codes  uint32 [B, Hkv, Lcap/64, 64, 8]. In block j (tokens 64j..64j+63), lane l = n + 16g and
-#         word w = 2*t4 + cc hold the 16 codes of token 64j + 16*t4 + n for dims 64cc + 16g + e,
-#         e = 4k + b, at bits 8b + 2k.
+#  codes  uint32 [B, Hkv, Lcap/64, 64, 4b] for a b-bit thumbnail. In block j (tokens 64j..64j+63),
+#         lane l = n + 16g holds, for token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims
+#         64cc + 16g + e (e = 4k + i, k, i in 0..3) in the b/2 words starting at (2*t4 + cc) * b/2:
+#         dim e sits in word (2*t4 + cc) * b/2 + k // (8/b), at bit 8i + b * (k % (8/b)). The field
+#         holds c for b = 2, 4 and the byte c - 128 (two's complement) for b = 8. For b = 2 this is
+#         word 2*t4 + cc, bit 8i + 2k.
 #  absmax bf16 [B, Hkv, Lcap/64, 16, 4]. Element [j, n, t4] is M of token 64j + 16*t4 + n.
-#  resid  int8 [B, Hkv, Lcap/16, 2, 64, 16]. Element [T, cc, n + 16g, e] is the residual of
-#         token 16T + n at dim 64cc + 16g + e.
+#  resid  int8 [B, Hkv, Lcap/16, 2, 64, 16]. Element [T, cc, n + 16g, e] is the residual of token
+#         16T + n at dim 64cc + 16g + e.
 # ------------------------------------------------------------------------------------------------
 
-def pack_codes(codes: np.ndarray) -> np.ndarray:
-    """Pack ``codes [Lcap, 128]`` (0..3) into the ``[Lcap/64, 64, 8]`` uint32 layout above."""
+def _code_field(c: int, bits: int) -> int:
+    """The stored field of code ``c``: ``c`` itself, or the byte ``c - 128`` for 8-bit codes."""
+    return (int(c) - 128) & 0xFF if bits == 8 else int(c)
+
+
+def pack_codes(codes: np.ndarray, bits: int = 2) -> np.ndarray:
+    """Pack ``codes [Lcap, 128]`` (``0 .. 2^b - 1``) into the ``[Lcap/64, 64, 4b]`` uint32 layout."""
     Lcap = codes.shape[0]
-    out = np.zeros((Lcap // 64, 64, 8), dtype=np.uint32)
-    c = np.asarray(codes, dtype=np.uint32)
+    per = 8 // bits                                   # codes per byte
+    out = np.zeros((Lcap // 64, 64, 4 * bits), dtype=np.uint32)
     for j in range(Lcap // 64):
         for g in range(4):
             for n in range(16):
                 for t4 in range(4):
                     t = 64 * j + 16 * t4 + n
                     for cc in range(2):
-                        word = 0
+                        w0 = (2 * t4 + cc) * (bits // 2)
                         for e in range(16):
-                            k, b = divmod(e, 4)
-                            word |= int(c[t, 64 * cc + 16 * g + e]) << (8 * b + 2 * k)
-                        out[j, n + 16 * g, 2 * t4 + cc] = word
+                            k, i = divmod(e, 4)
+                            w = w0 + k // per
+                            f = _code_field(codes[t, 64 * cc + 16 * g + e], bits)
+                            out[j, n + 16 * g, w] |= np.uint32(f << (8 * i + bits * (k % per)))
     return out
 
 
-def unpack_codes(packed: np.ndarray, Lcap: int) -> np.ndarray:
+def unpack_codes(packed: np.ndarray, Lcap: int, bits: int = 2) -> np.ndarray:
     """Inverse of :func:`pack_codes`."""
-    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 64, 64, 8)
+    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 64, 64, 4 * bits)
+    per = 8 // bits
     codes = np.zeros((Lcap, 128), dtype=np.int64)
     for j in range(Lcap // 64):
         for g in range(4):
             for n in range(16):
                 for t4 in range(4):
                     for cc in range(2):
-                        word = int(packed[j, n + 16 * g, 2 * t4 + cc])
+                        w0 = (2 * t4 + cc) * (bits // 2)
                         for e in range(16):
-                            k, b = divmod(e, 4)
-                            codes[64 * j + 16 * t4 + n, 64 * cc + 16 * g + e] = (word >> (8 * b + 2 * k)) & 3
+                            k, i = divmod(e, 4)
+                            word = int(packed[j, n + 16 * g, w0 + k // per])
+                            f = (word >> (8 * i + bits * (k % per))) & (2 ** bits - 1)
+                            c = (f + 128) & 0xFF if bits == 8 else f
+                            codes[64 * j + 16 * t4 + n, 64 * cc + 16 * g + e] = c
     return codes
 
 
-def pack_codes_fast(codes: np.ndarray) -> np.ndarray:
+def pack_codes_fast(codes: np.ndarray, bits: int = 2) -> np.ndarray:
     """Vectorised :func:`pack_codes` (checked equal to the loop form on small inputs)."""
     Lcap = codes.shape[0]
-    c = np.asarray(codes, dtype=np.uint32).reshape(Lcap // 64, 4, 16, 2, 4, 4, 4)  # j,t4,n,cc,g,k,b
-    c = c.transpose(0, 4, 2, 1, 3, 5, 6)                                           # j,g,n,t4,cc,k,b
-    shift = (8 * np.arange(4)[None, :] + 2 * np.arange(4)[:, None]).astype(np.uint32)  # [k, b]
-    words = np.bitwise_or.reduce((c << shift).reshape(*c.shape[:5], 16), axis=-1)
-    return words.reshape(Lcap // 64, 64, 8).astype(np.uint32)
+    per = 8 // bits
+    c = np.asarray(codes, dtype=np.int64)
+    f = ((c - 128) & 0xFF) if bits == 8 else c
+    # axes: j, t4, n, cc, g, (k // per), (k % per), i
+    f = f.astype(np.uint32).reshape(Lcap // 64, 4, 16, 2, 4, bits // 2, per, 4)
+    f = f.transpose(0, 4, 2, 1, 3, 5, 6, 7)           # j, g, n, t4, cc, k // per, k % per, i
+    shift = (8 * np.arange(4)[None, :] + bits * np.arange(per)[:, None]).astype(np.uint32)
+    words = np.bitwise_or.reduce((f << shift).reshape(*f.shape[:6], 4 * per), axis=-1)
+    return words.reshape(Lcap // 64, 64, 4 * bits).astype(np.uint32)
 
 
 def pack_absmax(M_bits: np.ndarray) -> np.ndarray:
@@ -380,26 +434,33 @@ def pack_resid(resid: np.ndarray) -> np.ndarray:
     return r.transpose(0, 2, 3, 1, 4).reshape(Lcap // 16, 2, 64, 16).copy()
 
 
-def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = None):
-    """Oracle for the quantization pass: packed ``(codes, absmax_bits, resid)`` for ``[B,Hkv,Lcap,128]``.
+def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = None, bits: int = 2):
+    """Oracle for the quantization pass: packed ``(codes, absmax_bits, resid)`` for ``[B,Hkv,Lcap,128]``
+    with a ``bits``-bit thumbnail.
 
     Only tokens in ``[t_begin, t_end)`` are defined; the others are returned as zero.
     """
     B, Hkv, Lcap, d = k_bits.shape
     t_end = Lcap if t_end is None else t_end
-    codes = np.zeros((B, Hkv, Lcap // 64, 64, 8), dtype=np.uint32)
+    codes = np.zeros((B, Hkv, Lcap // 64, 64, 4 * bits), dtype=np.uint32)
     absmax = np.zeros((B, Hkv, Lcap // 64, 16, 4), dtype=np.uint16)
     resid = np.zeros((B, Hkv, Lcap // 16, 2, 64, 16), dtype=np.int8)
+    live = np.zeros(Lcap, dtype=bool)
+    live[t_begin:t_end] = True
     for b in range(B):
         for h in range(Hkv):
             K = bf16_to_f64(k_bits[b, h])
-            c, M, r = quantize_keys(K)
-            live = np.zeros(Lcap, dtype=bool)
-            live[t_begin:t_end] = True
+            c, M, r = quantize_keys(K, bits)
             c = np.where(live[:, None], c, 0)
             r = np.where(live[:, None], r, 0)
             Mb = np.where(live, f64_to_bf16_bits(M), 0).astype(np.uint16)
-            codes[b, h] = pack_codes_fast(c)
+            packed = pack_codes_fast(c, bits)
+            if bits == 8:                             # tokens outside the range hold zero words
+                dead = ~live.reshape(Lcap // 64, 4, 16).transpose(0, 2, 1)   # j, n, t4
+                packed = packed.reshape(Lcap // 64, 4, 16, 4, 2, 4)          # j, g, n, t4, cc, k
+                packed[np.broadcast_to(dead[:, None, :, :, None, None], packed.shape)] = 0
+                packed = packed.reshape(Lcap // 64, 64, 32)
+            codes[b, h] = packed
             absmax[b, h] = pack_absmax(Mb)
             resid[b, h] = pack_resid(r)
     return codes, absmax, resid
