@@ -14,7 +14,8 @@ the tokens in blocks kept by any head of a KV group, queries, outputs and split 
 by the step time. ``roofline`` is the dominant kernel's algorithmic bandwidth from per-kernel HIP
 events (recorded by the library between its kernels, in separate eager steps), with its HBM
 traffic from the committed rocprofv3 counter record. ``stream_ceiling`` measures a plain device copy
-under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep.
+under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep. ``depth_sweep`` times the
+same step with 4- and 8-bit thumbnails (the 4+8 and 8+8 depths of App. C) beside the 2+8 headline.
 """
 from __future__ import annotations
 
@@ -31,7 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, AMD published
-SCAN_BYTES_PER_TOKEN = 32 + 2         # 2-bit codes for 128 dims + bf16 absmax
+SCAN_BYTES_PER_TOKEN = 32 + 2         # 2-bit codes for 128 dims + bf16 absmax (16 b + 2 for b bits)
 GATHER_BYTES_PER_TOKEN = 128 + 256    # int8 residual + bf16 values
 DENSE_BYTES_PER_TOKEN = 256 + 256     # bf16 keys + values
 METRIC = ("µs/decode step + effective HBM TB/s at 128K ctx; speedup vs dense flash-decode")
@@ -56,6 +57,8 @@ def parse():
                     help="comma-separated context lengths in K (e.g. 4,8,16,32,64,128,256): "
                          "workload 2's layout at each length, FFD vs dense")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--depths", default="4,8",
+                    help="wider thumbnail depths timed beside the 2-bit headline (App. C), '' for none")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed FFD steps only (for rocprofv3 runs)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -64,15 +67,16 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(case, mask, S):
-    """Bytes one FFD step must move, counted from the measured per-head block mask."""
+def algorithmic_bytes(case, mask, S, bits=2):
+    """Bytes one FFD step must move, counted from the measured per-head block mask (b-bit codes)."""
     G, D = case.G, case.D
+    scan_per_token = SCAN_BYTES_PER_TOKEN + 16 * (bits - 2)
     scan = 0
     gather_tokens = 0
     for b in range(case.B):
         L = int(case.seq_lens[b])
         nb = -(-L // 64)
-        scan += SCAN_BYTES_PER_TOKEN * L * case.Hkv
+        scan += scan_per_token * L * case.Hkv
         for h in range(case.Hkv):
             union = mask[b, h * G:(h + 1) * G, :nb].any(axis=0)
             toks = union.astype(np.int64) * 64
@@ -286,6 +290,34 @@ def decode_loop(r, delta, steps, warmup):
                     "the graph is captured once and replayed while the cache grows"}
 
 
+def depth_sweep(r, delta, depths, steps, dense_us):
+    """The step with b-bit thumbnails (App. C's 4+8 and 8+8): the cache quantized at that depth,
+    the step timed as the headline, and the three kernels timed by library events."""
+    torch, ffd, c = r.torch, r.ffd, r.case
+    saved = r.qk
+    out = {}
+    for bits in depths:
+        r.qk = ffd.empty_quantized(c.B, c.Hkv, c.Lcap, r.dev, bits)
+        ffd.quantize_keys(r.k, out=r.qk)
+        keep = r.mask_for(delta)
+        nb = algorithmic_bytes(c, keep, r.S, bits)
+        ms, _ = r.time(lambda: r.ffd_step(delta), steps, 5)
+        _, _, st = r.time(lambda ev: r.ffd_step(delta, events=ev), steps, 3, stages=True)
+        su = st.mean(axis=0) * 1e3
+        us = float(ms.mean() * 1e3)
+        scan_bytes = nb["scan"] + c.B * c.Hq * 2 * c.D
+        out[f"{bits}+8"] = {"us": round(us, 2), "scan_us": round(float(su[0]), 2),
+                            "refine_us": round(float(su[1]), 2), "merge_us": round(float(su[2]), 2),
+                            "scan_bytes": int(scan_bytes),
+                            "scan_gbps": round(scan_bytes / (float(su[0]) * 1e-6) / 1e9, 1),
+                            "keep_head_blocks": round(float(keep.mean()), 5),
+                            "speedup_vs_dense": round(dense_us / us, 2)}
+        r.qk = None
+        torch.cuda.empty_cache()
+    r.qk = saved
+    return out
+
+
 def stream_ceiling(r, reps=10):
     """Plain read (float32 sum) and plain copy of 512 MiB under the bench's flush protocol."""
     torch = r.torch
@@ -386,6 +418,8 @@ def main():
                          "speedup_vs_dense": round(dense_us / su, 2)}
 
     ceiling = stream_ceiling(r)
+    depths = depth_sweep(r, args.delta, [int(x) for x in args.depths.split(",") if x.strip()],
+                         20, dense_us)
     loop = decode_loop(r, args.delta, min(args.steps, 60), 10)      # writes the caches: run last
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
@@ -433,6 +467,9 @@ def main():
         "dense_tbps": round(dbytes / (dense_us * 1e-6) / 1e12, 3),
         "speedup_vs_dense": round(dense_us / us, 2),
         "delta_sweep": sweep,
+        "depth_sweep": {"2+8": {"us": round(eager_us, 2), "scan_us": round(float(stage_us[0]), 2),
+                                "refine_us": round(float(stage_us[1]), 2),
+                                "merge_us": round(float(stage_us[2]), 2)}, **depths},
         "stream_ceiling": ceiling,
         "decode_loop": loop,
         "quantize_cache_us": round(r.quant_ms * 1e3, 1),

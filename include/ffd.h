@@ -3,11 +3,12 @@
  *
  * One decode step of grouped-query attention for a batch of sequences:
  *
- *   ffd_quantize_keys           split each key into a 2-bit thumbnail and an 8-bit residual
- *                               (Sec. 3.1; App. A formulation; Fig. 2 "K quantization").
+ *   ffd_quantize_keys           split each key into a b-bit thumbnail and an 8-bit residual
+ *                               (Sec. 3.1; App. A formulation; Fig. 2 "K quantization"; b = 2, or
+ *                               4 and 8 for the wider depths of App. C).
  *   ffd_append_kv               append one decode token per sequence to the bf16 and quantized
  *                               caches at its device-side length, and advance the length.
- *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), 2-bit scan and
+ *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), b-bit scan and
  *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement that reuses
  *                               the scan dot products (Eq. 4), online-softmax attention over the kept
  *                               blocks, split into partial states merged by log-sum-exp
@@ -29,15 +30,23 @@
  *  - Pointers must be 16-byte aligned. Argument checks run before any launch; on failure nothing is
  *    enqueued and an ffd_status error is returned. A failed launch returns FFD_ERR_HIP.
  *
+ * Thumbnail depth. `thumb_bits` b is 2 (the method's 2+8 format), 4 or 8 (the 4+8 and 8+8 depths of
+ * App. C); any other positive value gives FFD_ERR_UNSUPPORTED. Code c in 0 .. 2^b - 1 stands for the
+ * level c - Lv, Lv = (2^b - 1) / 2, on the step s = M / Lv. The same b must be used to write the
+ * cache (ffd_quantize_keys, ffd_append_kv) and to read it (ffd_decode_attention).
+ *
  * Quantized-key storage (this library's format; the paper fixes none). Per (b, kvh):
- *  - codes  uint32 [Lcap/64][64][8]: block j = tokens 64j..64j+63; lane l = n + 16g and word
- *           w = 2*t4 + cc hold the 16 codes of token 64j + 16*t4 + n for dims 64cc + 16g + e,
- *           e = 4k + b, at bits 8b + 2k. Code c in {0,1,2,3} stands for level c - 1.5.
+ *  - codes  uint32 [Lcap/64][64][4b]: block j = tokens 64j..64j+63; lane l = n + 16g holds, for
+ *           token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims 64cc + 16g + e, e = 4k + i,
+ *           in the b/2 words from (2*t4 + cc) * b/2: dim e in word (2*t4 + cc) * b/2 + k / (8/b) at
+ *           bit 8i + b * (k % (8/b)). The field holds c for b = 2, 4 and the byte c - 128 (two's
+ *           complement) for b = 8. For b = 2: word 2*t4 + cc, bit 8i + 2k.
  *  - absmax bf16 [Lcap/64][16][4]: element [j][n][t4] = M = max_i |k_i| of token 64j + 16*t4 + n.
  *  - resid  int8 [Lcap/16][2][64][16]: element [T][cc][n + 16g][e] is the residual of token 16T + n
  *           at dim 64cc + 16g + e.
- *  The reconstruction is k ~= M * n / 381 with n = 254 c + r - 381 (thumbnail step M/1.5,
- *  residual step M/(1.5*254)); the thumbnail alone is k^quant = (c - 1.5) * M / 1.5.
+ *  The reconstruction is k ~= M * n / (254 Lv) with n = 254 c + r - 254 Lv (thumbnail step M/Lv,
+ *  residual step M/(254 Lv)); the thumbnail alone is k^quant = (c - Lv) * M / Lv. For b = 2:
+ *  k ~= M * n / 381 and k^quant = (c - 1.5) * M / 1.5.
  */
 #ifndef FFD_H
 #define FFD_H
@@ -64,9 +73,10 @@ typedef enum {
 
 /*
  * Key quantization (Sec. 3.1: k -> {k^quant, k^res}; App. A: symmetric mid-rise 2-bit codebook
- * {-1.5,-0.5,0.5,1.5}, s = max|k|/1.5, nearest level; ties at bin edges go to the upper level).
- * Residual: r = rint(381 k / M) - 254 c + 381 in [-127, 127] (round half to even); M = 0 gives
- * code 2 and residual 0.
+ * {-1.5,-0.5,0.5,1.5}, s = max|k|/1.5, nearest level; ties at bin edges go to the upper level;
+ * App. C: the same scheme with 2^b levels for b = 4, 8). Residual: r = rint(254 Lv k / M) - 254 c
+ * + 254 Lv in [-127, 127] (round half to even; for b = 2, rint(381 k / M) - 254 c + 381); M = 0
+ * gives code 2^(b-1) (level +0.5) and residual 0. Exact for every finite bf16 key.
  *
  *   k         bf16  [B, Hkv, Lcap, D]      keys (read)
  *   k_codes   uint32 codes layout above    (written for tokens [t_begin, t_end) only)
@@ -76,7 +86,8 @@ typedef enum {
  *   decode-step token is t_begin = L, t_end = L + 1.
  */
 int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resid,
-                      int B, int Hkv, int Lcap, int D, int t_begin, int t_end, hipStream_t stream);
+                      int B, int Hkv, int Lcap, int D, int thumb_bits, int t_begin, int t_end,
+                      hipStream_t stream);
 
 /*
  * Decode-step append, the cache update before attention in each step of a decode loop (the cache
@@ -90,19 +101,20 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
  *
  *   k_new, v_new   bf16 [B, Hkv, D]          the new token's key and value (read)
  *   k_cache, v_cache  bf16 [B, Hkv, Lcap, D]  or NULL
- *   k_codes, k_absmax, k_resid                quantized key layouts above
+ *   k_codes, k_absmax, k_resid                quantized key layouts above, b = thumb_bits
  *   seq_lens       int32 [B] (device, read and written)
  */
 int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, void* k_codes,
                   void* k_absmax, void* k_resid, int32_t* seq_lens, int B, int Hkv, int Lcap, int D,
-                  hipStream_t stream);
+                  int thumb_bits, hipStream_t stream);
 
 /*
  * FFD decode attention (Alg. 1 with Eq. 1-4), one query per head.
  *
  *   q            bf16  [B, Hq, D]
- *   k_codes, k_absmax, k_resid   quantized keys (from ffd_quantize_keys)
+ *   k_codes, k_absmax, k_resid   quantized keys (from ffd_quantize_keys with the same thumb_bits)
  *   v            bf16  [B, Hkv, Lcap, D]
+ *   thumb_bits   thumbnail depth b of the codes (2, 4 or 8); the scan reads 16b bytes per token
  *   seq_lens     int32 [B] (device)
  *   block_size   must be 64
  *   delta        top-delta margin >= 0 (+inf keeps every block); a block j is kept for head h iff
@@ -130,8 +142,8 @@ int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_c
  */
 int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax,
                          const void* k_resid, const void* v, const int32_t* seq_lens,
-                         int B, int Hq, int Hkv, int Lcap, int D, int block_size, float delta,
-                         int n_sink, int n_local, int num_splits, float softmax_scale,
+                         int B, int Hq, int Hkv, int Lcap, int D, int thumb_bits, int block_size,
+                         float delta, int n_sink, int n_local, int num_splits, float softmax_scale,
                          void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -143,8 +155,8 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
  */
 int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
                                 const void* k_resid, const void* v, const int32_t* seq_lens,
-                                int B, int Hq, int Hkv, int Lcap, int D, int block_size, float delta,
-                                int n_sink, int n_local, int num_splits, float softmax_scale,
+                                int B, int Hq, int Hkv, int Lcap, int D, int thumb_bits, int block_size,
+                                float delta, int n_sink, int n_local, int num_splits, float softmax_scale,
                                 void* out, float* lse, uint8_t* block_mask,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream,
                                 hipEvent_t* stage_events);

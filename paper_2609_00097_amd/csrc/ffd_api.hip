@@ -39,6 +39,12 @@ int check_shapes(int B, int Hq, int Hkv, int Lcap, int D) {
     return FFD_OK;
 }
 
+// Thumbnail depths with kernels: 2+8 (App. A), 4+8 and 8+8 (App. C).
+int check_bits(int bits) {
+    if (bits == 2 || bits == 4 || bits == 8) return FFD_OK;
+    return bits > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
+}
+
 int launch_status() {
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? FFD_OK : FFD_ERR_HIP;
@@ -161,8 +167,9 @@ const char* ffd_status_string(int status) {
 }
 
 int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resid, int B, int Hkv,
-                      int Lcap, int D, int t_begin, int t_end, hipStream_t stream) {
+                      int Lcap, int D, int thumb_bits, int t_begin, int t_end, hipStream_t stream) {
     int st = check_shapes(B, Hkv, Hkv, Lcap, D);
+    if (st == FFD_OK) st = check_bits(thumb_bits);
     if (st != FFD_OK) return st;
     if (t_begin < 0 || t_end < t_begin || t_end > Lcap) return FFD_ERR_INVALID_ARGUMENT;
     if (B == 0 || t_end == t_begin) return FFD_OK;
@@ -171,15 +178,21 @@ int ffd_quantize_keys(const void* k, void* k_codes, void* k_absmax, void* k_resi
         return FFD_ERR_INVALID_ARGUMENT;
     QuantArgs a{static_cast<const uint16_t*>(k), static_cast<uint32_t*>(k_codes),
                 static_cast<uint16_t*>(k_absmax), static_cast<int8_t*>(k_resid), Hkv, Lcap, t_begin, t_end};
-    const dim3 grid((unsigned)((t_end - t_begin + 15) / 16), (unsigned)Hkv, (unsigned)B);
-    hipLaunchKernelGGL(quantize_keys_kernel, grid, dim3(kThreads), 0, stream, a);
+    const dim3 grid((unsigned)((t_end - (t_begin & ~63) + 63) / 64), (unsigned)Hkv, (unsigned)B);
+    if (thumb_bits == 2)
+        hipLaunchKernelGGL(quantize_keys_kernel<2>, grid, dim3(kThreads), 0, stream, a);
+    else if (thumb_bits == 4)
+        hipLaunchKernelGGL(quantize_keys_kernel<4>, grid, dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(quantize_keys_kernel<8>, grid, dim3(kThreads), 0, stream, a);
     return launch_status();
 }
 
 int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, void* k_codes,
                   void* k_absmax, void* k_resid, int32_t* seq_lens, int B, int Hkv, int Lcap, int D,
-                  hipStream_t stream) {
+                  int thumb_bits, hipStream_t stream) {
     int st = check_shapes(B, Hkv, Hkv, Lcap, D);
+    if (st == FFD_OK) st = check_bits(thumb_bits);
     if (st != FFD_OK) return st;
     if (B == 0) return FFD_OK;
     if (!k_new || !v_new || !k_codes || !k_absmax || !k_resid || !seq_lens) return FFD_ERR_INVALID_ARGUMENT;
@@ -191,20 +204,27 @@ int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_c
                  static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
                  static_cast<uint32_t*>(k_codes), static_cast<uint16_t*>(k_absmax),
                  static_cast<int8_t*>(k_resid), seq_lens, Hkv, Lcap};
-    hipLaunchKernelGGL(append_kv_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, a);
+    if (thumb_bits == 2)
+        hipLaunchKernelGGL(append_kv_kernel<2>, dim3((unsigned)B), dim3(kThreads), 0, stream, a);
+    else if (thumb_bits == 4)
+        hipLaunchKernelGGL(append_kv_kernel<4>, dim3((unsigned)B), dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(append_kv_kernel<8>, dim3((unsigned)B), dim3(kThreads), 0, stream, a);
     return launch_status();
 }
 
 int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
                                 const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
-                                int Hkv, int Lcap, int D, int block_size, float delta, int n_sink,
+                                int Hkv, int Lcap, int D, int thumb_bits, int block_size, float delta, int n_sink,
                                 int n_local, int num_splits, float softmax_scale, void* out, float* lse,
                                 uint8_t* block_mask, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream, hipEvent_t* stage_events) {
     if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
     if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
     int S = 0;
-    int st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
+    int st = check_bits(thumb_bits);
+    if (st != FFD_OK) return st;
+    st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
                                      lse, workspace, workspace_bytes, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
@@ -231,7 +251,8 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
                 Lcap, G, S1, delta, scale, n_sink, n_local};
     RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_absmax),
                   static_cast<const int8_t*>(k_resid), static_cast<const uint16_t*>(v), seq_lens, lists,
-                  counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale};
+                  counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale,
+                  thumb_top_level(thumb_bits)};
     const dim3 scan_grid((unsigned)S1, (unsigned)Hkv, (unsigned)B);
     const dim3 refine_grid((unsigned)(Wr + npairs));
     auto mark = [&](int i) {
@@ -239,10 +260,13 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
     };
 
     if ((st = mark(0)) != FFD_OK) return st;
-    if (G <= 4)
-        hipLaunchKernelGGL(ffd_scan_kernel<1>, scan_grid, dim3(kThreads), 0, stream, sa);
+    auto scan = [&](auto kernel) { hipLaunchKernelGGL(kernel, scan_grid, dim3(kThreads), 0, stream, sa); };
+    if (thumb_bits == 2)
+        G <= 4 ? scan(ffd_scan_kernel<1, 2>) : scan(ffd_scan_kernel<2, 2>);
+    else if (thumb_bits == 4)
+        G <= 4 ? scan(ffd_scan_kernel<1, 4>) : scan(ffd_scan_kernel<2, 4>);
     else
-        hipLaunchKernelGGL(ffd_scan_kernel<2>, scan_grid, dim3(kThreads), 0, stream, sa);
+        G <= 4 ? scan(ffd_scan_kernel<1, 8>) : scan(ffd_scan_kernel<2, 8>);
     if ((st = launch_status()) != FFD_OK || (st = mark(1)) != FFD_OK) return st;
     if (G <= 4)
         hipLaunchKernelGGL(ffd_refine_kernel<1>, refine_grid, dim3(kThreads), 0, stream, ra);
@@ -257,11 +281,11 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
 
 int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absmax, const void* k_resid,
                          const void* v, const int32_t* seq_lens, int B, int Hq, int Hkv, int Lcap, int D,
-                         int block_size, float delta, int n_sink, int n_local, int num_splits,
+                         int thumb_bits, int block_size, float delta, int n_sink, int n_local, int num_splits,
                          float softmax_scale, void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
     return ffd_decode_attention_events(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
-                                       block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
+                                       thumb_bits, block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
                                        lse, block_mask, workspace, workspace_bytes, stream, nullptr);
 }
 

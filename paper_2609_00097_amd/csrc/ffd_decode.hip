@@ -1,5 +1,5 @@
-// FFD decode attention for gfx950: 2-bit scan + top-delta selection, then refinement + online
-// softmax over the kept blocks.
+// FFD decode attention for gfx950: b-bit thumbnail scan (b = 2, 4, 8; App. C) + top-delta
+// selection, then refinement + online softmax over the kept blocks.
 //
 // Method (Alg. 1; Eq. 1-4): for each query head h of a KV group,
 //   s_hat[t] = alpha * q . k^quant_t                      (thumbnail scan)
@@ -10,11 +10,12 @@
 //
 // Arithmetic. The group's queries are the A operand of v_mfma_i32_16x16x64_i8: each query is held in
 // fixed point Q = rint(q * 2^(22-E)) (|q| < 2^E), split into three signed 8-bit limbs, one MFMA row
-// per (head, limb). The B operand is either a 16-token tile's 2-bit codes expanded to bytes (two VALU
-// ops per 4 codes) or its stored int8 residual, so both dot products are exact integer sums,
-// combined and rounded once to fp32:
-//   sum_d Q_d (2 c_d - 3) = T  (int32, exact),     s_hat = T * M_t * alpha 2^(E-23) / 1.5
-//   sum_d Q_d r_d         = R  (three int32 limbs), z = s_hat + R * M_t * alpha 2^(E-22) / 381
+// per (head, limb). The B operand is either a 16-token tile's codes as bytes (2- and 4-bit codes
+// expanded by two VALU ops per 4 codes, 8-bit codes stored as the signed bytes c - 128) or its stored
+// int8 residual, so both dot products are exact integer sums, combined and rounded once to fp32:
+//   sum_d Q_d (2 c_d - (2^b - 1)) = T  (exact: int32 for b = 2, int64 otherwise),
+//                                   s_hat = T * M_t * alpha 2^(E-23) / Lv,   Lv = (2^b - 1) / 2
+//   sum_d Q_d r_d                 = R  (three int32 limbs), z = s_hat + R * M_t * alpha 2^(E-22) / (254 Lv)
 // Output register i of lane (g, n) is row 4g + i, column n: head g's limbs for token n, so each
 // 16-lane row group owns one head and a tile's maximum is a 16-lane DPP reduction.
 //
@@ -45,8 +46,8 @@ namespace {
 #ifndef FFD_REFINE_OCC
 #define FFD_REFINE_OCC 3
 #endif
-constexpr int kRing = FFD_SCAN_RING;          // scan loads in flight per wave (blocks)
-constexpr int kPMW = 2;                       // pseudo-max window blocks per wave per pass
+constexpr int kRing2 = FFD_SCAN_RING;         // 2-bit scan loads in flight per wave (blocks)
+constexpr int kPMW2 = 2;                      // 2-bit pseudo-max window blocks per wave per pass
 constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
 constexpr int kChunk = kFfdChunk;             // list entries staged per pass of the refinement kernel
 constexpr int kWaveList = kFfdMaxScanBlocks / kWaves;   // kept blocks one scan wave can hold
@@ -59,28 +60,40 @@ __device__ __forceinline__ int limb_of(int Q, int which) {
     return which == 0 ? l0 : (which == 1 ? l1 : l2);
 }
 
-__device__ __forceinline__ v4i expand_codes(uint32_t w) {
+// The 16 codes of one (tile, 64-dim chunk) group of a lane, from its b/2 words, as the MFMA B
+// operand: byte i of dword k is dim 4k + i of the lane's 16-dim slice.
+template <int BITS>
+__device__ __forceinline__ v4i expand_codes(const uint32_t* w) {
     v4i r;
-    r.x = (int)(w & 0x03030303u);
-    r.y = (int)((w >> 2) & 0x03030303u);
-    r.z = (int)((w >> 4) & 0x03030303u);
-    r.w = (int)((w >> 6) & 0x03030303u);
+    if constexpr (BITS == 2) {
+        r.x = (int)(w[0] & 0x03030303u);
+        r.y = (int)((w[0] >> 2) & 0x03030303u);
+        r.z = (int)((w[0] >> 4) & 0x03030303u);
+        r.w = (int)((w[0] >> 6) & 0x03030303u);
+    } else if constexpr (BITS == 4) {
+        r.x = (int)(w[0] & 0x0f0f0f0fu);
+        r.y = (int)((w[0] >> 4) & 0x0f0f0f0fu);
+        r.z = (int)(w[1] & 0x0f0f0f0fu);
+        r.w = (int)((w[1] >> 4) & 0x0f0f0f0fu);
+    } else {
+        r.x = (int)w[0]; r.y = (int)w[1]; r.z = (int)w[2]; r.w = (int)w[3];
+    }
     return r;
 }
 
 template <int NT>
 struct HeadConsts {
     v4i A[NT][2];      // MFMA A operand per head tile and 64-dim chunk
-    int off[NT];       // 3 * sum_d Q_d of head 4t + g
-    float kap[NT];     // alpha * 2^(E-23) / 1.5
-    float kap2[NT];    // alpha * 2^(E-22) / 381
+    int sumq[NT];      // sum_d Q_d of head 4t + g
+    float kap[NT];     // alpha * 2^(E-23) / Lv
+    float kap2[NT];    // alpha * 2^(E-22) / (254 Lv)
     bool live[NT];     // head 4t + g exists
 };
 
 template <int NT>
 struct QueryLds {
     alignas(16) int8_t limbs[4][4 * NT][kD];     // [limb][head][dim]; limb 3 is zero
-    int off[4 * NT];
+    int sumq[4 * NT];
     float kap[4 * NT];
     float kap2[4 * NT];
 };
@@ -96,10 +109,11 @@ __device__ __forceinline__ void load_query_words(const uint16_t* __restrict__ q,
 
 // Queries -> fixed-point limbs in LDS and this lane's per-head constants. Head h (wave h % 4): E with
 // max|q| < 2^E, Q = rint(q 2^(22-E)) split into three signed bytes stored as limbs[limb][h][d]; the
-// fourth limb row and heads past G stay zero. Contains two workgroup barriers.
+// fourth limb row and heads past G stay zero. lv is the thumbnail's outer level Lv. Contains two
+// workgroup barriers.
 template <int NT>
 __device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint32_t (&qw)[NT], int G,
-                                                   float scale, int tid, HeadConsts<NT>& hc) {
+                                                   float scale, float lv, int tid, HeadConsts<NT>& hc) {
     const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, n = lane & 15;
     for (int i = tid; i < 4 * 4 * NT * kD / 4; i += kThreads) reinterpret_cast<int*>(sm.limbs)[i] = 0;
     __syncthreads();
@@ -120,9 +134,9 @@ __device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint3
         }
         const int sum = wave_sum_i(Q0 + Q1);
         if (lane == 0) {
-            sm.off[h] = 3 * sum;
-            sm.kap[h] = ldexpf(scale / 1.5f, E - 23);
-            sm.kap2[h] = ldexpf(scale / 381.f, E - 22);
+            sm.sumq[h] = sum;
+            sm.kap[h] = ldexpf(scale / lv, E - 23);
+            sm.kap2[h] = ldexpf(scale / (254.f * lv), E - 22);
         }
     }
     __syncthreads();
@@ -135,50 +149,68 @@ __device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint3
             hc.A[t][cc] = *reinterpret_cast<const v4i*>(&sm.limbs[limb][hrow][64 * cc + 16 * g]);
         const int hh = 4 * t + g;      // this lane's output head
         hc.live[t] = hh < G;
-        hc.off[t] = hc.live[t] ? sm.off[hh] : 0;
+        hc.sumq[t] = hc.live[t] ? sm.sumq[hh] : 0;
         hc.kap[t] = hc.live[t] ? sm.kap[hh] : 0.f;
         hc.kap2[t] = hc.live[t] ? sm.kap2[hh] : 0.f;
     }
 }
 
-// One lane's share of a block's thumbnail: 32 B of codes (both 64-dim halves of its token in each
-// of the four tiles) and the absmax of its four tokens.
+// One lane's share of a block's thumbnail: 16b bytes of codes (both 64-dim halves of its token in
+// each of the four tiles) and the absmax of its four tokens.
+template <int BITS>
 struct BlockScan {
-    uint4 w0, w1;
+    uint4 w[BITS];
     uint2 mm;
 };
 
-__device__ __forceinline__ BlockScan load_block_scan(const uint32_t* __restrict__ codes_bh,
-                                                     const uint16_t* __restrict__ absmax_bh, int j,
-                                                     int lane) {
-    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + ((size_t)j * 64 + lane) * 2;
-    BlockScan r;
-    r.w0 = cp[0];
-    r.w1 = cp[1];
+template <int BITS>
+__device__ __forceinline__ BlockScan<BITS> load_block_scan(const uint32_t* __restrict__ codes_bh,
+                                                           const uint16_t* __restrict__ absmax_bh, int j,
+                                                           int lane) {
+    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + ((size_t)j * 64 + lane) * BITS;
+    BlockScan<BITS> r;
+#pragma unroll
+    for (int i = 0; i < BITS; ++i) r.w[i] = cp[i];
     r.mm = *reinterpret_cast<const uint2*>(absmax_bh + (size_t)j * 64 + (lane & 15) * 4);
     return r;
 }
 
 // Thumbnail scores of block j for this lane's head(s) and tokens 64j + 16*T4 + n; -inf past L.
-template <int NT>
-__device__ __forceinline__ void block_scores(const BlockScan& ld, int j, int lane, int L,
+// Lane words of tile T4, chunk cc start at word (2 T4 + cc) b/2 (the storage layout of ffd.h).
+template <int NT, int BITS>
+__device__ __forceinline__ void block_scores(const BlockScan<BITS>& ld, int j, int lane, int L,
                                              const HeadConsts<NT>& hc, float (&sc)[NT][4]) {
     const int n = lane & 15;
     const float M[4] = {bf16_lo(ld.mm.x), bf16_hi(ld.mm.x), bf16_lo(ld.mm.y), bf16_hi(ld.mm.y)};
-    const uint32_t words[8] = {ld.w0.x, ld.w0.y, ld.w0.z, ld.w0.w, ld.w1.x, ld.w1.y, ld.w1.z, ld.w1.w};
+    uint32_t words[4 * BITS];
+#pragma unroll
+    for (int i = 0; i < BITS; ++i) {
+        words[4 * i] = ld.w[i].x; words[4 * i + 1] = ld.w[i].y;
+        words[4 * i + 2] = ld.w[i].z; words[4 * i + 3] = ld.w[i].w;
+    }
 #pragma unroll
     for (int T4 = 0; T4 < 4; ++T4) {
-        const v4i b0 = expand_codes(words[2 * T4 + 0]);
-        const v4i b1 = expand_codes(words[2 * T4 + 1]);
+        const v4i b0 = expand_codes<BITS>(&words[(2 * T4 + 0) * (BITS / 2)]);
+        const v4i b1 = expand_codes<BITS>(&words[(2 * T4 + 1) * (BITS / 2)]);
         const bool valid = 64 * j + 16 * T4 + n < L;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             v4i acc = {0, 0, 0, 0};
             acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], b0, acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], b1, acc, 0, 0, 0);
-            const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
-            const int T = (int)(2u * s - (uint32_t)hc.off[t]);     // exact modulo 2^32, |T| < 2^31
-            sc[t][T4] = valid ? (float)T * (M[T4] * hc.kap[t]) : -INFINITY;
+            float Tf;
+            if constexpr (BITS == 2) {
+                // |sum_d Q_d (2 c_d - 3)| <= 3 * 128 * 2^22 < 2^31: exact modulo 2^32
+                const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
+                Tf = (float)(int)(2u * s - 3u * (uint32_t)hc.sumq[t]);
+            } else {
+                const long long s = (long long)acc.x + ((long long)acc.y << 8) + ((long long)acc.z << 16);
+                // 8-bit codes are the bytes c - 128, and 2c - 255 = 2 (c - 128) + 1
+                const long long T = BITS == 8 ? 2 * s + hc.sumq[t]
+                                              : 2 * s - (long long)((1 << BITS) - 1) * hc.sumq[t];
+                Tf = (float)T;
+            }
+            sc[t][T4] = valid ? Tf * (M[T4] * hc.kap[t]) : -INFINITY;
         }
     }
 }
@@ -267,13 +299,21 @@ struct RefineLds {
 }  // namespace
 
 // ================================================================================================
-// Scan: pseudo-max, 2-bit scan, keep decision; scan scores and the kept list to the workspace.
+// Scan: pseudo-max, b-bit thumbnail scan, keep decision; scan scores and the kept list to the
+// workspace.
 // Grid (S1, Hkv, B); workgroup s1 scans blocks [s1 * bps, (s1 + 1) * bps) of one (sequence, KV
 // head), bps = ceil(nblk / S1) <= kFfdMaxScanBlocks; wave w takes a contiguous quarter of them and
 // keeps kRing blocks in flight.
 // ================================================================================================
-template <int NT>
-__global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
+// Loads in flight per wave: a ring of blocks and the pseudo-max window blocks of a pass, fewer for the
+// wider thumbnails (whose blocks are 2x and 4x larger).
+template <int BITS> constexpr int scan_ring() { return BITS == 2 ? kRing2 : 2; }
+template <int BITS> constexpr int scan_pmw() { return BITS == 8 ? 1 : kPMW2; }
+
+template <int NT, int BITS>
+__global__ __launch_bounds__(kThreads, BITS == 8 ? 2 : 4) void ffd_scan_kernel(ScanArgs a) {
+    constexpr int kRing = scan_ring<BITS>();
+    constexpr int kPMW = scan_pmw<BITS>();
     __shared__ ScanLds<NT> sm;
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -290,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
         return;
     }
 
-    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * 8;
+    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * BITS);
     const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
     float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
 
@@ -312,16 +352,17 @@ __global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
     const int loc_blk_beg = max(loc_beg / kBlock, sink_blk_end);
     const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
-    BlockScan win[kPMW];
+    BlockScan<BITS> win[kPMW];
 #pragma unroll
     for (int i = 0; i < kPMW; ++i)
-        win[i] = load_block_scan(codes_bh, absmax_bh, min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
-    BlockScan ring[kRing];
+        win[i] = load_block_scan<BITS>(codes_bh, absmax_bh,
+                                       min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
+    BlockScan<BITS> ring[kRing];
 #pragma unroll
-    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
+    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
 
     HeadConsts<NT> hc;
-    build_query_consts<NT>(sm.qs, qw, G, a.scale, tid, hc);
+    build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
 
     // ---- pseudo-max over sink and local windows (Eq. 3) ----------------------------------
     float pm[NT];
@@ -331,14 +372,14 @@ __global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
         if (base > 0) {
 #pragma unroll
             for (int i = 0; i < kPMW; ++i)
-                win[i] = load_block_scan(codes_bh, absmax_bh, pm_block(min(base + kWaves * i + wave, npm - 1)), lane);
+                win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, pm_block(min(base + kWaves * i + wave, npm - 1)), lane);
         }
 #pragma unroll
         for (int i = 0; i < kPMW; ++i) {
             const int idx = base + kWaves * i + wave;
             const int j = pm_block(min(idx, npm - 1));
             float sc[NT][4];
-            block_scores<NT>(win[i], j, lane, L, hc, sc);
+            block_scores<NT, BITS>(win[i], j, lane, L, hc, sc);
 #pragma unroll
             for (int T4 = 0; T4 < 4; ++T4) {
                 const int tok = 64 * j + 16 * T4 + n;
@@ -365,9 +406,9 @@ __global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
 
     // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
     int nkept = 0;                                  // wave-uniform
-    auto decide = [&](const BlockScan& blk, int j) {
+    auto decide = [&](const BlockScan<BITS>& blk, int j) {
         float sc[NT][4];
-        block_scores<NT>(blk, j, lane, L, hc, sc);
+        block_scores<NT, BITS>(blk, j, lane, L, hc, sc);
         uint32_t bits = 0;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -398,7 +439,7 @@ __global__ __launch_bounds__(kThreads, 4) void ffd_scan_kernel(ScanArgs a) {
         for (int r = 0; r < kRing; ++r) {
             const int j = jw0 + i0 + r;
             decide(ring[r], j);
-            ring[r] = load_block_scan(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
+            ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
         }
     }
 #pragma unroll
@@ -621,7 +662,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
             sm.u.list[i] = list_bh[lo * bps + (r - (pref[lo] - pref0))];
         }
         if (!consts_ready) {                        // the query loads and the list loads overlap
-            build_query_consts<NT>(sm.qs, qw, G, a.scale, tid, hc);
+            build_query_consts<NT>(sm.qs, qw, G, a.scale, a.top_level, tid, hc);
             consts_ready = true;
         }
         __syncthreads();
@@ -648,8 +689,12 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                        a.part_l, a.part_acc);
 }
 
-template __global__ void ffd_scan_kernel<1>(ScanArgs);
-template __global__ void ffd_scan_kernel<2>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 2>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8>(ScanArgs);
 template __global__ void ffd_refine_kernel<1>(RefineArgs);
 template __global__ void ffd_refine_kernel<2>(RefineArgs);
 

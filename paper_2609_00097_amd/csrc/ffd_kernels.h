@@ -13,9 +13,13 @@ constexpr int kFfdChunk = 1024;
 constexpr int kFfdMaxScanBlocks = 256;
 constexpr int kFfdMaxScanSplits = 1024;
 
+// Thumbnail depth b (App. C: 2+8, 4+8, 8+8): 2^b levels c - Lv, Lv = (2^b - 1) / 2; a token's codes
+// take 4b words.
+__host__ __device__ constexpr float thumb_top_level(int bits) { return ((1 << bits) - 1) * 0.5f; }
+
 struct ScanArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
-    const uint32_t* codes;      // [B, Hkv, Lcap/64, 64, 8]
+    const uint32_t* codes;      // [B, Hkv, Lcap/64, 64, 4b] (b = the kernel's thumbnail depth)
     const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
     const int32_t* seq_lens;    // [B]
     uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, per scan split
@@ -42,6 +46,7 @@ struct RefineArgs {
     float* part_acc;            // [(W + B*Hkv) * G, 128]
     int Hq, Hkv, Lcap, G, S1, W, npairs;
     float scale;
+    float top_level;            // Lv of the thumbnail depth: the residual step is M / (254 Lv)
 };
 
 struct DenseArgs {
@@ -76,11 +81,11 @@ struct AppendArgs {
     int Hkv, Lcap;
 };
 
-template <int NT> __global__ void ffd_scan_kernel(ScanArgs a);
+template <int NT, int BITS> __global__ void ffd_scan_kernel(ScanArgs a);
 template <int NT> __global__ void ffd_refine_kernel(RefineArgs a);
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
-__global__ void quantize_keys_kernel(QuantArgs a);
-__global__ void append_kv_kernel(AppendArgs a);
+template <int BITS> __global__ void quantize_keys_kernel(QuantArgs a);
+template <int BITS> __global__ void append_kv_kernel(AppendArgs a);
 __global__ void lse_merge_kernel(const float* part_m, const float* part_l, const float* part_acc, int S,
                                  const int2* table, int G, uint16_t* out, float* lse);
 

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libffd.so")
 HEAD_DIM = 128
 BLOCK = 64
 MAX_SPLITS = 1024
+THUMB_BITS = (2, 4, 8)      # thumbnail depths: 2+8 (the method), 4+8 and 8+8 (App. C)
 STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
           3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
 
@@ -53,9 +54,9 @@ def lib() -> ctypes.CDLL:
         so = ctypes.CDLL(LIB_PATH)
     except OSError as e:
         raise FfdLibraryError(f"cannot load {LIB_PATH}: {e}") from e
-    so.ffd_quantize_keys.argtypes = [P, P, P, P, I, I, I, I, I, I, P]
-    so.ffd_append_kv.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, P]
-    so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, I, I, F,
+    so.ffd_quantize_keys.argtypes = [P, P, P, P, I, I, I, I, I, I, I, P]
+    so.ffd_append_kv.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, P]
+    so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, F, I, I, I, F,
                                         P, P, P, P, SZ, P]
     so.ffd_decode_attention_events.argtypes = so.ffd_decode_attention.argtypes + [P]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
@@ -115,31 +116,56 @@ def new_workspace(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0, dev
                        dtype=torch.uint8, device=device)
 
 
-def quantized_shapes(B: int, Hkv: int, Lcap: int):
-    """Shapes of (codes int32, absmax bf16, resid int8) for a cache of capacity Lcap."""
-    return ((B, Hkv, Lcap // 64, 64, 8), (B, Hkv, Lcap // 64, 16, 4), (B, Hkv, Lcap // 16, 2, 64, 16))
+def quantized_shapes(B: int, Hkv: int, Lcap: int, bits: int = 2):
+    """Shapes of (codes int32, absmax bf16, resid int8) for a cache of capacity Lcap with a
+    ``bits``-bit thumbnail."""
+    return ((B, Hkv, Lcap // 64, 64, 4 * bits), (B, Hkv, Lcap // 64, 16, 4),
+            (B, Hkv, Lcap // 16, 2, 64, 16))
 
 
-def empty_quantized(B: int, Hkv: int, Lcap: int, device):
-    sc, sa, sr = quantized_shapes(B, Hkv, Lcap)
+def thumb_bits(codes: torch.Tensor) -> int:
+    """The thumbnail depth of a codes tensor, from its last dimension (4 words per bit)."""
+    bits = codes.shape[-1] // 4 if codes.dim() == 5 else 0
+    if bits not in THUMB_BITS or codes.shape[-1] != 4 * bits:
+        raise ValueError(f"codes must be [B, Hkv, Lcap/64, 64, 4b] with b in {THUMB_BITS}, "
+                         f"got {tuple(codes.shape)}")
+    return bits
+
+
+def empty_quantized(B: int, Hkv: int, Lcap: int, device, bits: int = 2):
+    sc, sa, sr = quantized_shapes(B, Hkv, Lcap, bits)
     return (torch.empty(sc, dtype=torch.int32, device=device),
             torch.empty(sa, dtype=torch.bfloat16, device=device),
             torch.empty(sr, dtype=torch.int8, device=device))
 
 
-def quantize_keys(k: torch.Tensor, t_begin: int = 0, t_end: int | None = None, out=None):
-    """Split bf16 keys ``[B, Hkv, Lcap, 128]`` into (codes, absmax, resid) for ``[t_begin, t_end)``."""
+def _need_quantized(quantized, B, Hkv, Lcap) -> int:
+    codes, absmax, resid = quantized
+    bits = thumb_bits(codes)
+    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
+                             (torch.int32, torch.bfloat16, torch.int8),
+                             quantized_shapes(B, Hkv, Lcap, bits)):
+        _need(t, nm, dt, sh)
+    return bits
+
+
+def quantize_keys(k: torch.Tensor, t_begin: int = 0, t_end: int | None = None, out=None,
+                  bits: int = 2):
+    """Split bf16 keys ``[B, Hkv, Lcap, 128]`` into (codes, absmax, resid) for ``[t_begin, t_end)``
+    with a ``bits``-bit thumbnail (2, 4 or 8; taken from ``out``'s codes shape when given)."""
     if k.dim() != 4:
         raise ValueError("k must be [B, Hkv, Lcap, 128]")
     B, Hkv, Lcap, D = k.shape
     _need(k, "k", torch.bfloat16)
     t_end = Lcap if t_end is None else t_end
-    codes, absmax, resid = out if out is not None else empty_quantized(B, Hkv, Lcap, k.device)
-    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
-                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
-        _need(t, nm, dt, sh)
+    if out is None:
+        if bits not in THUMB_BITS:
+            raise ValueError(f"bits must be one of {THUMB_BITS}")
+        out = empty_quantized(B, Hkv, Lcap, k.device, bits)
+    bits = _need_quantized(out, B, Hkv, Lcap)
+    codes, absmax, resid = out
     _check("ffd_quantize_keys", lib().ffd_quantize_keys(
-        _ptr(k), _ptr(codes), _ptr(absmax), _ptr(resid), B, Hkv, Lcap, D, t_begin, t_end,
+        _ptr(k), _ptr(codes), _ptr(absmax), _ptr(resid), B, Hkv, Lcap, D, bits, t_begin, t_end,
         _stream(k.device)))
     return codes, absmax, resid
 
@@ -154,15 +180,13 @@ def append_kv(k_new, v_new, quantized, seq_lens, *, k_cache=None, v_cache=None):
     _need(k_new, "k_new", torch.bfloat16)
     _need(v_new, "v_new", torch.bfloat16, (B, Hkv, D))
     _need(seq_lens, "seq_lens", torch.int32, (B,))
-    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
-                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
-        _need(t, nm, dt, sh)
+    bits = _need_quantized(quantized, B, Hkv, Lcap)
     for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache")):
         if t is not None:
             _need(t, nm, torch.bfloat16, (B, Hkv, Lcap, D))
     _check("ffd_append_kv", lib().ffd_append_kv(
         _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(codes), _ptr(absmax), _ptr(resid),
-        _ptr(seq_lens), B, Hkv, Lcap, D, _stream(k_new.device)))
+        _ptr(seq_lens), B, Hkv, Lcap, D, bits, _stream(k_new.device)))
 
 
 def _attn_outputs(q, B, Hq, Lcap, want_lse, want_mask, out, lse, mask):
@@ -179,6 +203,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
                      return_lse: bool = True, return_mask: bool = False, workspace=None,
                      out=None, lse=None, mask=None, stage_events=None):
     """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested).
+    The thumbnail depth is that of ``codes`` (its last dimension is 4 words per bit).
 
     ``stage_events``: optional four ``torch.cuda.Event`` objects, already recorded once (so that
     they exist), which the library records before the scan kernel, after it, after the refinement
@@ -188,9 +213,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
     _need(q, "q", torch.bfloat16)
     _need(v, "v", torch.bfloat16, (B, Hkv, Lcap, D))
     _need(seq_lens, "seq_lens", torch.int32, (B,))
-    for t, nm, dt, sh in zip((codes, absmax, resid), ("codes", "absmax", "resid"),
-                             (torch.int32, torch.bfloat16, torch.int8), quantized_shapes(B, Hkv, Lcap)):
-        _need(t, nm, dt, sh)
+    bits = _need_quantized((codes, absmax, resid), B, Hkv, Lcap)
     out, lse, mask = _attn_outputs(q, B, Hq, Lcap, return_lse or lse is not None,
                                    return_mask or mask is not None, out, lse, mask)
     if workspace is None:
@@ -202,7 +225,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
         ev = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
     _check("ffd_decode_attention", lib().ffd_decode_attention_events(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
-        D, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
+        D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
         _ptr(lse), _ptr(mask), _ptr(workspace), workspace.numel() * workspace.element_size(),
         _stream(q.device), ev))
     return out, lse, mask

@@ -48,14 +48,15 @@ def check_lse(name, gpu, ref, tol=LSE_TOL):
     assert not bad.any(), f"{name}: lse mismatch at {np.argwhere(bad)[:5].tolist()} gpu {gpu[bad][:5]} ref {ref[bad][:5]}"
 
 
-def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local=None):
+def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local=None, bits=2):
     """Masks bit-exact outside the near-threshold band; outputs/lse against the oracle on the
-    GPU's own mask. Returns (number of near-threshold blocks, number of mismatches inside it)."""
+    GPU's own mask (thumbnail depth ``bits``). Returns (number of near-threshold blocks, number of
+    mismatches inside it)."""
     n_sink = case.n_sink if n_sink is None else n_sink
     n_local = case.n_local if n_local is None else n_local
     gmask = mask.cpu().numpy().astype(bool)
     ref = O.decode_batch(case.q, case.k, case.v, case.seq_lens, delta=delta, n_sink=n_sink,
-                         n_local=n_local, heads=heads)
+                         n_local=n_local, heads=heads, bits=bits)
     G = case.G
     pairs = heads if heads is not None else [(b, h) for b in range(case.B) for h in range(case.Hkv)]
     rows = [(b, h * G + i) for b, h in pairs for i in range(G)]
@@ -65,7 +66,7 @@ def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local
     diff = gmask[bi, hi] != ref["keep"][bi, hi]
     assert not (diff & ~near).any(), f"mask mismatch outside the near-threshold band at {np.argwhere(diff & ~near)[:5].tolist()}"
     on_mask = O.decode_batch(case.q, case.k, case.v, case.seq_lens, delta=delta, n_sink=n_sink,
-                             n_local=n_local, keep=gmask, heads=heads)
+                             n_local=n_local, keep=gmask, heads=heads, bits=bits)
     check_close("out", bf16_to_f64(out)[bi, hi], on_mask["out"][bi, hi])
     if lse is not None:
         check_lse("lse", lse.cpu().numpy()[bi, hi], on_mask["lse"][bi, hi])

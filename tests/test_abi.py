@@ -66,7 +66,7 @@ def test_splits_and_workspace_sizes(so):
 
 def _decode(so, **kw):
     a = dict(q=None, codes=None, absmax=None, resid=None, v=None, lens=None, B=1, Hq=32, Hkv=8,
-             Lcap=4096, D=128, block=64, delta=5.0, n_sink=64, n_local=256, splits=0, scale=0.0,
+             Lcap=4096, D=128, bits=2, block=64, delta=5.0, n_sink=64, n_local=256, splits=0, scale=0.0,
              out=None, lse=None, mask=None, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return so.ffd_decode_attention(*a.values())
@@ -77,6 +77,8 @@ def _decode(so, **kw):
     (dict(D=96), 2), (dict(block=32), 2), (dict(Hq=12, Hkv=1), 2), (dict(Hq=30), 1),
     (dict(Lcap=100), 1), (dict(delta=-1.0), 1), (dict(delta=float("nan")), 1),
     (dict(n_sink=-1), 1), (dict(splits=2000), 1), (dict(B=0), 0),
+    (dict(bits=3), 2), (dict(bits=16), 2), (dict(bits=0), 1), (dict(bits=-2), 1),
+    (dict(B=0, bits=4), 0), (dict(B=0, bits=8), 0), (dict(B=0, bits=1), 2),
 ])
 def test_argument_checks_return_before_any_launch(so, kw, status):
     assert _decode(so, **kw) == status
@@ -96,16 +98,19 @@ def test_misaligned_and_small_workspace(so):
 def test_append_argument_checks(so):
     fake = 0x1000
     # null pointers, misalignment, bad shapes: rejected before any launch
-    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 1, 8, 4096, 128, None) == 1
-    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake + 2, 1, 8, 4096, 128, None) == 1
-    assert so.ffd_append_kv(fake, fake + 8, None, None, fake, fake, fake, fake, 1, 8, 4096, 128, None) == 1
-    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 100, 128, None) == 1
-    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 4096, 96, None) == 2
-    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 0, 8, 4096, 128, None) == 0
+    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 1, 8, 4096, 128, 2, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake + 2, 1, 8, 4096, 128, 2, None) == 1
+    assert so.ffd_append_kv(fake, fake + 8, None, None, fake, fake, fake, fake, 1, 8, 4096, 128, 2, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 100, 128, 2, None) == 1
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 4096, 96, 2, None) == 2
+    assert so.ffd_append_kv(fake, fake, None, None, fake, fake, fake, fake, 1, 8, 4096, 128, 3, None) == 2
+    assert so.ffd_append_kv(None, None, None, None, None, None, None, None, 0, 8, 4096, 128, 8, None) == 0
 
 
 def test_quantize_range_checks(so):
-    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 10, 5, None) == 1
-    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 0, 5000, None) == 1
-    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 7, 7, None) == 0
-    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 96, 0, 1, None) == 2
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 2, 10, 5, None) == 1
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 2, 0, 5000, None) == 1
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, 2, 7, 7, None) == 0
+    assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 96, 2, 0, 1, None) == 2
+    for bits, status in ((4, 0), (8, 0), (3, 2), (0, 1)):
+        assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, bits, 7, 7, None) == status
