@@ -23,7 +23,9 @@ Readings of the paper taken where it is silent or ambiguous (each is listed in t
   ``n = rint(254 Lv k / M)`` and ``r = n - 254 c + 254 Lv``. ``b = 2`` is the formulation above.
 * All scores (scan, pseudo-max, block score, refined logits) carry the ``1/sqrt(d)`` of Eq. 1.
 * The pseudo-max (Alg. 1; Eq. 3) is taken over thumbnail scores of the first ``n_sink`` tokens and
-  the last ``n_local`` tokens of the sequence.
+  the last ``n_local`` tokens of the sequence. Eq. 3's own reading (the window tokens' true scores)
+  is available as a variant: ``pm_source="refined"`` (thumbnail + residual, Eq. 4's logits) or
+  ``"exact"`` (the bf16 keys themselves).
 * A block is tokens ``[B*j, min(B*j + B, L))``; only valid tokens enter its score and the softmax.
 * Masks are per query head; a KV head's residual/values are read for the union over its group.
 * An empty selection or an empty sequence gives output 0 and ``lse = -inf``.
@@ -144,6 +146,22 @@ def pseudo_max_tokens(L: int, n_sink: int, n_local: int) -> np.ndarray:
     return np.union1d(sink, local).astype(np.int64)
 
 
+PM_SOURCES = ("thumbnail", "refined", "exact")
+
+
+def window_scores(source, s_hat, z, q, K, L, alpha):
+    """The scores the pseudo-max is taken over: the thumbnail scores (Alg. 1, the default), the
+    refined logits (thumbnail + residual, Eq. 4), or the exact scores of the bf16 keys (Eq. 3's
+    ``s_it``). Only the window tokens' entries are used."""
+    if source == "thumbnail":
+        return s_hat
+    if source == "refined":
+        return z
+    if source == "exact":
+        return alpha * (np.asarray(q, dtype=np.float64) @ np.asarray(K[:L], dtype=np.float64).T)
+    raise ValueError(f"pm_source must be one of {PM_SOURCES}")
+
+
 def pseudo_max(s_hat: np.ndarray, L: int, n_sink: int, n_local: int) -> np.ndarray:
     """``m~_h = max(max_{S_global} s_hat, max_{S_local} s_hat)`` per head; ``-inf`` if both are empty."""
     idx = pseudo_max_tokens(L, n_sink, n_local)
@@ -245,29 +263,33 @@ def lse_merge(states):
 # The whole decode step for one (sequence, KV head) group, and for a batch.
 # ------------------------------------------------------------------------------------------------
 
-def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None, bits=2):
+def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None, bits=2,
+                 pm_source="thumbnail"):
     """FFD decode for the ``G`` query heads ``q [G, d]`` sharing keys ``K [Lcap, d]``, values ``V``.
 
     Follows Alg. 1 in order: quantize, pseudo-max, top-delta selection, refinement, softmax . V.
     When ``keep`` (bool ``[G, nblk]``) is given, attention runs on that mask instead of the
     oracle's own selection (used to compare outputs given the GPU's mask). ``bits`` is the
-    thumbnail depth (App. C).
+    thumbnail depth (App. C); ``pm_source`` the scores the pseudo-max is taken over
+    (:func:`window_scores`).
     """
     codes, M, resid = quantize_keys(K[:L], bits)
     return decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=n_sink,
-                                  n_local=n_local, block=block, alpha=alpha, keep=keep, bits=bits)
+                                  n_local=n_local, block=block, alpha=alpha, keep=keep, bits=bits,
+                                  pm_source=pm_source, K=K)
 
 
 def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, block, alpha,
-                           keep=None, bits=2):
+                           keep=None, bits=2, pm_source="thumbnail", K=None):
     """The decode step of :func:`decode_group` given the already quantized keys (Alg. 1 from the
-    pseudo-max on; the quantization happens when the cache is written, Fig. 2)."""
+    pseudo-max on; the quantization happens when the cache is written, Fig. 2). ``K`` (the exact
+    keys) is needed only for ``pm_source="exact"``."""
     s_hat = scan_scores(q, codes, M, alpha, bits)
-    m_tilde = pseudo_max(s_hat, L, n_sink, n_local)
+    z_all = refined_logits(q, codes, M, resid, alpha, bits)
+    m_tilde = pseudo_max(window_scores(pm_source, s_hat, z_all, q, K, L, alpha), L, n_sink, n_local)
     sigma = block_scores(s_hat, L, block)
     own_keep = select_blocks(sigma, m_tilde, delta)
     use = own_keep if keep is None else np.asarray(keep, dtype=bool)[:, :sigma.shape[1]]
-    z_all = refined_logits(q, codes, M, resid, alpha, bits)
     outs, lses = [], []
     for h in range(q.shape[0]):
         tok = token_mask_from_blocks(use[h], L, block)
@@ -279,13 +301,13 @@ def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, 
 
 
 def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, block=64,
-                 softmax_scale=None, keep=None, heads=None, bits=2):
+                 softmax_scale=None, keep=None, heads=None, bits=2, pm_source="thumbnail"):
     """FFD decode for a batch. Inputs are bf16 bit patterns ``q [B,Hq,d]``, ``k, v [B,Hkv,Lcap,d]``.
 
     Returns float64 ``out [B,Hq,d]``, ``lse [B,Hq]``, the per-head block mask ``keep [B,Hq,nblk]``
     (blocks at or beyond a sequence's end are False), ``sigma`` and ``m_tilde``.
     ``heads`` optionally restricts work to a list of ``(b, kvh)`` pairs (others left as NaN);
-    ``bits`` is the thumbnail depth (App. C).
+    ``bits`` is the thumbnail depth (App. C), ``pm_source`` the pseudo-max's scores.
     """
     B, Hq, d = q_bits.shape
     Hkv, Lcap = k_bits.shape[1], k_bits.shape[2]
@@ -311,7 +333,7 @@ def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, bl
         V = bf16_to_f64(v_bits[b, h, :L])
         kb = None if keep is None else np.asarray(keep[b, sl], dtype=bool)
         r = decode_group(q, K, V, L, delta=delta, n_sink=n_sink, n_local=n_local, block=block,
-                         alpha=alpha, keep=kb, bits=bits)
+                         alpha=alpha, keep=kb, bits=bits, pm_source=pm_source)
         nb = r["sigma"].shape[1]
         out[b, sl] = r["out"]
         lse[b, sl] = r["lse"]
@@ -338,6 +360,43 @@ def dense_batch(q_bits, k_bits, v_bits, seq_lens, *, softmax_scale=None, heads=N
         out[b, sl] = o
         lse[b, sl] = l
     return dict(out=out, lse=lse)
+
+
+# ------------------------------------------------------------------------------------------------
+# Fidelity diagnostics (Sec. 5.1 recall and LSE error; Sec. 5.2 pseudo-max gap).
+# ------------------------------------------------------------------------------------------------
+
+def exact_max(q, K, L, alpha):
+    """``m_h = max_{t < L} alpha q_h . k_t``, the true maximum score the pseudo-max estimates
+    (Sec. 5.2); ``-inf`` for an empty sequence."""
+    if L == 0:
+        return np.full(np.asarray(q).shape[0], -np.inf)
+    return np.max(alpha * (np.asarray(q, dtype=np.float64) @ np.asarray(K[:L], dtype=np.float64).T), axis=1)
+
+
+def pseudo_max_gap(m, m_tilde):
+    """``m - m~`` per head (Sec. 5.2, Fig. 5); 0 where both are ``-inf``."""
+    m, mt = np.asarray(m, dtype=np.float64), np.asarray(m_tilde, dtype=np.float64)
+    with np.errstate(invalid="ignore"):
+        return np.where(np.isneginf(m) & np.isneginf(mt), 0.0, m - mt)
+
+
+def recall_cosine(out, ref):
+    """Sec. 5.1 recall: the cosine similarity of the sparse output and the dense output, per head
+    (the last axis is the head dimension); 1 where both are zero."""
+    a, b = np.asarray(out, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    na, nb = np.linalg.norm(a, axis=-1), np.linalg.norm(b, axis=-1)
+    dot = np.sum(a * b, axis=-1)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        c = dot / (na * nb)
+    return np.where((na == 0) & (nb == 0), 1.0, c)
+
+
+def lse_abs_error(lse, ref):
+    """Sec. 5.1 LSE error: ``|lse - lse_dense|`` per head (0 where both are ``-inf``)."""
+    a, b = np.asarray(lse, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    with np.errstate(invalid="ignore"):
+        return np.where(np.isneginf(a) & np.isneginf(b), 0.0, np.abs(a - b))
 
 
 def near_threshold(sigma, m_tilde, delta, band=1e-3):
