@@ -16,6 +16,8 @@ events (recorded by the library between its kernels, in separate eager steps), w
 traffic from the committed rocprofv3 counter record. ``stream_ceiling`` measures a plain device copy
 under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep. ``depth_sweep`` times the
 same step with 4- and 8-bit thumbnails (the 4+8 and 8+8 depths of App. C) beside the 2+8 headline.
+``fidelity`` gives Sec. 5.1's recall (cosine with the dense output) and LSE error and Sec. 5.2's
+pseudo-max gap m - m~ for each delta, with the pseudo-max over thumbnail or refined window scores.
 """
 from __future__ import annotations
 
@@ -57,6 +59,7 @@ def parse():
                     help="comma-separated context lengths in K (e.g. 4,8,16,32,64,128,256): "
                          "workload 2's layout at each length, FFD vs dense")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-fidelity", action="store_true", help="skip the fidelity diagnostics")
     ap.add_argument("--depths", default="4,8",
                     help="wider thumbnail depths timed beside the 2-bit headline (App. C), '' for none")
     ap.add_argument("--profile-only", action="store_true",
@@ -318,6 +321,59 @@ def depth_sweep(r, delta, depths, steps, dense_us):
     return out
 
 
+def exact_max(r):
+    """m = max_t alpha q.k_t per head over the exact bf16 keys (float32 products on the GPU; a
+    diagnostic computed with torch, outside the library)."""
+    torch, c = r.torch, r.case
+    alpha = 1.0 / math.sqrt(c.D)
+    m = torch.empty((c.B, c.Hq), dtype=torch.float32, device=r.dev)
+    for b in range(c.B):
+        L = int(c.seq_lens[b])
+        if L == 0:
+            m[b] = float("-inf")
+            continue
+        kf = r.k[b, :, :L].float()                                         # [Hkv, L, D]
+        qf = r.q[b].float().view(c.Hkv, c.G, c.D).transpose(1, 2).contiguous()   # [Hkv, D, G]
+        m[b] = (torch.matmul(kf, qf).amax(dim=1) * alpha).reshape(c.Hq)
+        del kf
+    return m
+
+
+def fidelity(r, deltas, steps):
+    """Sec. 5.1 recall (cosine of the FFD and dense outputs per head) and LSE error, Sec. 5.2 gap
+    m - m~ per head, keep ratio, and the step time, for each delta and pseudo-max source."""
+    torch, ffd, c = r.torch, r.ffd, r.case
+    r.dense_step()
+    d_out, d_lse = r.out.float().cpu().numpy(), r.lse.cpu().numpy()
+    m = exact_max(r).cpu().numpy()
+    mt = torch.empty((c.B, c.Hq), dtype=torch.float32, device=r.dev)
+    res = {}
+    for pm in ("thumbnail", "refined"):
+        for d in deltas:
+            ffd.decode_attention(r.q, *r.qk, r.v, r.lens, delta=d, n_sink=c.n_sink, n_local=c.n_local,
+                                 num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse, mask=r.mask,
+                                 m_tilde=mt, pseudo_max=pm)
+            torch.cuda.synchronize()
+            o, l = r.out.float().cpu().numpy(), r.lse.cpu().numpy()
+            keep = r.mask.cpu().numpy().astype(bool)
+            cos = np.sum(o * d_out, -1) / (np.linalg.norm(o, axis=-1) * np.linalg.norm(d_out, axis=-1))
+            err = np.abs(l - d_lse)
+            gap = m - mt.cpu().numpy()
+            ms, _ = r.time(lambda: ffd.decode_attention(
+                r.q, *r.qk, r.v, r.lens, delta=d, n_sink=c.n_sink, n_local=c.n_local,
+                num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse, pseudo_max=pm), steps, 3)
+            res[f"{pm}/delta={d:g}"] = {
+                "us": round(float(ms.mean() * 1e3), 2),
+                "keep_head_blocks": round(float(keep.mean()), 5),
+                "recall_min": round(float(cos.min()), 6), "recall_mean": round(float(cos.mean()), 6),
+                "lse_err_max": round(float(err.max()), 5), "lse_err_mean": round(float(err.mean()), 5),
+                "gap_p50_p90_max": [round(float(np.percentile(gap, p)), 4) for p in (50, 90, 100)],
+                "gap_zero_frac": round(float(np.mean(gap <= 0)), 4)}
+    return {"what": "FFD vs the dense kernel's output (cosine per head, |lse - lse_dense|), "
+                    "m - m~ with m the exact max over all tokens (float32 on the GPU); 128 heads",
+            **res}
+
+
 def stream_ceiling(r, reps=10):
     """Plain read (float32 sum) and plain copy of 512 MiB under the bench's flush protocol."""
     torch = r.torch
@@ -420,6 +476,7 @@ def main():
     ceiling = stream_ceiling(r)
     depths = depth_sweep(r, args.delta, [int(x) for x in args.depths.split(",") if x.strip()],
                          20, dense_us)
+    fid = None if args.no_fidelity else fidelity(r, [3.0, 5.0, 7.0], 20)
     loop = decode_loop(r, args.delta, min(args.steps, 60), 10)      # writes the caches: run last
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
@@ -471,6 +528,7 @@ def main():
                                 "refine_us": round(float(stage_us[1]), 2),
                                 "merge_us": round(float(stage_us[2]), 2)}, **depths},
         "stream_ceiling": ceiling,
+        "fidelity": fid,
         "decode_loop": loop,
         "quantize_cache_us": round(r.quant_ms * 1e3, 1),
         "wall_s_timed_region": round(wall, 3),

@@ -147,19 +147,40 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
                          void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Pseudo-max sources (ffd_decode_extras.pseudo_max). */
+#define FFD_PSEUDO_MAX_THUMBNAIL 0   /* m~ over the window tokens' thumbnail scores (Alg. 1; default) */
+#define FFD_PSEUDO_MAX_REFINED 1     /* m~ over their refined logits, thumbnail + residual (Eq. 3's
+                                        window scores read with the 8-bit residual, Eq. 4) */
+
 /*
- * ffd_decode_attention with stage timing, for measurement: when stage_events is not NULL it must
- * point to four events created by the caller (hipEventCreate); they are recorded on `stream` before
- * the scan kernel, between scan and refinement, between refinement and merge, and after the merge.
- * Everything else is as for ffd_decode_attention (which is this call with stage_events = NULL).
+ * Optional inputs and outputs of ffd_decode_attention_ex, for measurement and diagnostics
+ * (Sec. 5.1, Sec. 5.2). A NULL pointer field, or a NULL extras pointer, leaves that feature off.
+ *   stage_events  four events created by the caller (hipEventCreate), recorded on `stream` before
+ *                 the scan kernel, between scan and refinement, between refinement and merge, and
+ *                 after the merge.
+ *   m_tilde       float [B, Hq] (device): the pseudo-max m~ of each head (-inf for an empty
+ *                 sequence or when both windows are empty), for the gap m - m~ of Sec. 5.2.
+ *   pseudo_max    FFD_PSEUDO_MAX_THUMBNAIL or FFD_PSEUDO_MAX_REFINED (other values:
+ *                 FFD_ERR_INVALID_ARGUMENT). The refined source reads the window blocks' residuals
+ *                 as well; the selection still compares thumbnail block scores with m~ - delta.
  */
-int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
-                                const void* k_resid, const void* v, const int32_t* seq_lens,
-                                int B, int Hq, int Hkv, int Lcap, int D, int thumb_bits, int block_size,
-                                float delta, int n_sink, int n_local, int num_splits, float softmax_scale,
-                                void* out, float* lse, uint8_t* block_mask,
-                                void* workspace, size_t workspace_bytes, hipStream_t stream,
-                                hipEvent_t* stage_events);
+typedef struct ffd_decode_extras {
+    hipEvent_t* stage_events;
+    float* m_tilde;
+    int pseudo_max;
+} ffd_decode_extras;
+
+/*
+ * ffd_decode_attention with the extras above; ffd_decode_attention is this call with extras = NULL.
+ * Everything else is as for ffd_decode_attention.
+ */
+int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_absmax,
+                            const void* k_resid, const void* v, const int32_t* seq_lens,
+                            int B, int Hq, int Hkv, int Lcap, int D, int thumb_bits, int block_size,
+                            float delta, int n_sink, int n_local, int num_splits, float softmax_scale,
+                            void* out, float* lse, uint8_t* block_mask,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream,
+                            const ffd_decode_extras* extras);
 
 /*
  * Exact dense decode attention over bf16 keys and values (the FlashAttention-2 comparator of

@@ -132,6 +132,27 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
     return FFD_OK;
 }
 
+// The scan kernel for this depth, head tiling and pseudo-max source.
+template <int NT, int BITS>
+void launch_scan_nt(bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (refined_pm)
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, true>), grid, dim3(kThreads), 0, stream, sa);
+    else
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, false>), grid, dim3(kThreads), 0, stream, sa);
+}
+
+template <int BITS>
+void launch_scan_bits(int nt, bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (nt == 1) launch_scan_nt<1, BITS>(refined_pm, grid, stream, sa);
+    else launch_scan_nt<2, BITS>(refined_pm, grid, stream, sa);
+}
+
+void launch_scan(int bits, int nt, bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (bits == 2) launch_scan_bits<2>(nt, refined_pm, grid, stream, sa);
+    else if (bits == 4) launch_scan_bits<4>(nt, refined_pm, grid, stream, sa);
+    else launch_scan_bits<8>(nt, refined_pm, grid, stream, sa);
+}
+
 }  // namespace
 
 extern "C" {
@@ -213,12 +234,17 @@ int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_c
     return launch_status();
 }
 
-int ffd_decode_attention_events(const void* q, const void* k_codes, const void* k_absmax,
-                                const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
-                                int Hkv, int Lcap, int D, int thumb_bits, int block_size, float delta, int n_sink,
-                                int n_local, int num_splits, float softmax_scale, void* out, float* lse,
-                                uint8_t* block_mask, void* workspace, size_t workspace_bytes,
-                                hipStream_t stream, hipEvent_t* stage_events) {
+int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_absmax,
+                            const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
+                            int Hkv, int Lcap, int D, int thumb_bits, int block_size, float delta, int n_sink,
+                            int n_local, int num_splits, float softmax_scale, void* out, float* lse,
+                            uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream, const ffd_decode_extras* extras) {
+    hipEvent_t* stage_events = extras ? extras->stage_events : nullptr;
+    float* m_tilde = extras ? extras->m_tilde : nullptr;
+    const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
+    if (pm_source != FFD_PSEUDO_MAX_THUMBNAIL && pm_source != FFD_PSEUDO_MAX_REFINED)
+        return FFD_ERR_INVALID_ARGUMENT;
     if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
     if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
     int S = 0;
@@ -229,6 +255,7 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
     if (st != FFD_OK || B == 0) return st;
     if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
     if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
+    if (m_tilde && (reinterpret_cast<uintptr_t>(m_tilde) & 3u)) return FFD_ERR_INVALID_ARGUMENT;
     if ((long long)B * Hkv > (1LL << 20)) return FFD_ERR_UNSUPPORTED;
     if (Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return FFD_ERR_UNSUPPORTED;
     if (workspace_bytes < ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)) return FFD_ERR_WORKSPACE_TOO_SMALL;
@@ -247,8 +274,8 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
     const int npairs = B * Hkv;
     const int Wr = S * npairs;
     ScanArgs sa{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
-                static_cast<const uint16_t*>(k_absmax), seq_lens, lists, counts, shat, block_mask, Hq, Hkv,
-                Lcap, G, S1, delta, scale, n_sink, n_local};
+                static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid), seq_lens, lists,
+                counts, shat, block_mask, m_tilde, Hq, Hkv, Lcap, G, S1, delta, scale, n_sink, n_local};
     RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_absmax),
                   static_cast<const int8_t*>(k_resid), static_cast<const uint16_t*>(v), seq_lens, lists,
                   counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale,
@@ -260,13 +287,7 @@ int ffd_decode_attention_events(const void* q, const void* k_codes, const void* 
     };
 
     if ((st = mark(0)) != FFD_OK) return st;
-    auto scan = [&](auto kernel) { hipLaunchKernelGGL(kernel, scan_grid, dim3(kThreads), 0, stream, sa); };
-    if (thumb_bits == 2)
-        G <= 4 ? scan(ffd_scan_kernel<1, 2>) : scan(ffd_scan_kernel<2, 2>);
-    else if (thumb_bits == 4)
-        G <= 4 ? scan(ffd_scan_kernel<1, 4>) : scan(ffd_scan_kernel<2, 4>);
-    else
-        G <= 4 ? scan(ffd_scan_kernel<1, 8>) : scan(ffd_scan_kernel<2, 8>);
+    launch_scan(thumb_bits, G <= 4 ? 1 : 2, pm_source == FFD_PSEUDO_MAX_REFINED, scan_grid, stream, sa);
     if ((st = launch_status()) != FFD_OK || (st = mark(1)) != FFD_OK) return st;
     if (G <= 4)
         hipLaunchKernelGGL(ffd_refine_kernel<1>, refine_grid, dim3(kThreads), 0, stream, ra);
@@ -284,9 +305,9 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
                          int thumb_bits, int block_size, float delta, int n_sink, int n_local, int num_splits,
                          float softmax_scale, void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    return ffd_decode_attention_events(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
-                                       thumb_bits, block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
-                                       lse, block_mask, workspace, workspace_bytes, stream, nullptr);
+    return ffd_decode_attention_ex(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
+                                   thumb_bits, block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
+                                   lse, block_mask, workspace, workspace_bytes, stream, nullptr);
 }
 
 int ffd_dense_decode_attention(const void* q, const void* k, const void* v, const int32_t* seq_lens, int B,

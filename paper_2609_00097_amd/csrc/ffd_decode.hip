@@ -310,8 +310,40 @@ struct RefineLds {
 template <int BITS> constexpr int scan_ring() { return BITS == 2 ? kRing2 : 2; }
 template <int BITS> constexpr int scan_pmw() { return BITS == 8 ? 1 : kPMW2; }
 
-template <int NT, int BITS>
-__global__ __launch_bounds__(kThreads, BITS == 8 ? 2 : 4) void ffd_scan_kernel(ScanArgs a) {
+// Adds the residual term of Eq. 4 to the thumbnail scores sc of block j (the refined logits of its
+// tokens, computed exactly as the refinement kernel computes them).
+template <int NT>
+__device__ __forceinline__ void add_residual_term(const int8_t* __restrict__ resid_bh, uint2 mm, int j,
+                                                  int lane, const HeadConsts<NT>& hc, float (&sc)[NT][4]) {
+    const float M[4] = {bf16_lo(mm.x), bf16_hi(mm.x), bf16_lo(mm.y), bf16_hi(mm.y)};
+    v4i r[4][2];
+#pragma unroll
+    for (int T4 = 0; T4 < 4; ++T4) {
+        const v4i* rp = reinterpret_cast<const v4i*>(resid_bh) + (size_t)(4 * j + T4) * 128 + lane;
+        r[T4][0] = rp[0];
+        r[T4][1] = rp[64];
+    }
+#pragma unroll
+    for (int T4 = 0; T4 < 4; ++T4) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            v4i acc = {0, 0, 0, 0};
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], r[T4][0], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], r[T4][1], acc, 0, 0, 0);
+            const float R = fmaf(65536.f, (float)acc.z, fmaf(256.f, (float)acc.y, (float)acc.x));
+            const float sct = sc[t][T4];
+            sc[t][T4] = sct == -INFINITY ? -INFINITY : fmaf(R, M[T4] * hc.kap2[t], sct);
+        }
+    }
+}
+
+// Workgroups per CU: the 8-bit blocks and the refined pseudo-max's residual tiles need more registers.
+template <int NT, int BITS, bool REFINED_PM> constexpr int scan_occupancy() {
+    return BITS == 8 ? 2 : (REFINED_PM ? (NT == 1 ? 3 : 2) : 4);
+}
+
+template <int NT, int BITS, bool REFINED_PM>
+__global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>())) void ffd_scan_kernel(ScanArgs a) {
     constexpr int kRing = scan_ring<BITS>();
     constexpr int kPMW = scan_pmw<BITS>();
     __shared__ ScanLds<NT> sm;
@@ -327,6 +359,7 @@ __global__ __launch_bounds__(kThreads, BITS == 8 ? 2 : 4) void ffd_scan_kernel(S
     const int jb = min(s * bps, nblk), je = min(jb + bps, nblk);
     if (jb >= je && !a.mask) {                  // nothing to scan (short sequence), nothing to clear
         if (tid == 0) a.counts[bh * a.S1 + s] = 0;
+        if (a.m_tilde && s == 0 && tid < G) a.m_tilde[(size_t)b * a.Hq + hq0 + tid] = -INFINITY;   // L = 0
         return;
     }
 
@@ -380,6 +413,8 @@ __global__ __launch_bounds__(kThreads, BITS == 8 ? 2 : 4) void ffd_scan_kernel(S
             const int j = pm_block(min(idx, npm - 1));
             float sc[NT][4];
             block_scores<NT, BITS>(win[i], j, lane, L, hc, sc);
+            if constexpr (REFINED_PM)
+                add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win[i].mm, j, lane, hc, sc);
 #pragma unroll
             for (int T4 = 0; T4 < 4; ++T4) {
                 const int tok = 64 * j + 16 * T4 + n;
@@ -402,6 +437,8 @@ __global__ __launch_bounds__(kThreads, BITS == 8 ? 2 : 4) void ffd_scan_kernel(S
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][4 * t + g]);
         thr[t] = m - a.delta;                      // -inf when both windows are empty
+        if (a.m_tilde && s == 0 && wave == 0 && n == 0 && hc.live[t])
+            a.m_tilde[(size_t)b * a.Hq + hq0 + 4 * t + g] = m;
     }
 
     // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
@@ -689,12 +726,18 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                        a.part_l, a.part_acc);
 }
 
-template __global__ void ffd_scan_kernel<1, 2>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 2>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 4>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 4>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 8>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 8>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 2, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8, false>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 2, true>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2, true>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4, true>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4, true>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8, true>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8, true>(ScanArgs);
 template __global__ void ffd_refine_kernel<1>(RefineArgs);
 template __global__ void ffd_refine_kernel<2>(RefineArgs);
 

@@ -21,11 +21,13 @@ struct ScanArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
     const uint32_t* codes;      // [B, Hkv, Lcap/64, 64, 4b] (b = the kernel's thumbnail depth)
     const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
+    const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]: read for the refined pseudo-max only
     const int32_t* seq_lens;    // [B]
     uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, per scan split
     int* counts;                // [B*Hkv, S1]: kept blocks per scan split
     float* shat;                // [B, Hkv, Lcap/64, 4, NT, 64]: scan scores of kept blocks
     uint8_t* mask;              // [B, Hq, Lcap/64] or null
+    float* m_tilde;             // [B, Hq] or null: the pseudo-max of each head
     int Hq, Hkv, Lcap, G, S1;
     float delta, scale;
     int n_sink, n_local;
@@ -81,7 +83,9 @@ struct AppendArgs {
     int Hkv, Lcap;
 };
 
-template <int NT, int BITS> __global__ void ffd_scan_kernel(ScanArgs a);
+// REFINED_PM: the pseudo-max is taken over the window tokens' refined logits (Eq. 3's reading)
+// instead of their thumbnail scores.
+template <int NT, int BITS, bool REFINED_PM> __global__ void ffd_scan_kernel(ScanArgs a);
 template <int NT> __global__ void ffd_refine_kernel(RefineArgs a);
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
 template <int BITS> __global__ void quantize_keys_kernel(QuantArgs a);

@@ -22,7 +22,7 @@ THUMB_BITS = (2, 4, 8)      # thumbnail depths: 2+8 (the method), 4+8 and 8+8 (A
 STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
           3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
 
-EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
+EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
            "ffd_dense_decode_attention",
            "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
@@ -41,6 +41,12 @@ class FfdError(RuntimeError):
 
 _lib = None
 P, I, F, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+PSEUDO_MAX = {"thumbnail": 0, "refined": 1}     # FFD_PSEUDO_MAX_THUMBNAIL, FFD_PSEUDO_MAX_REFINED
+
+
+class DecodeExtras(ctypes.Structure):
+    """``ffd_decode_extras``: stage events, the pseudo-max output and the pseudo-max source."""
+    _fields_ = [("stage_events", P), ("m_tilde", P), ("pseudo_max", I)]
 
 
 def lib() -> ctypes.CDLL:
@@ -58,7 +64,7 @@ def lib() -> ctypes.CDLL:
     so.ffd_append_kv.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, P]
     so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, F, I, I, I, F,
                                         P, P, P, P, SZ, P]
-    so.ffd_decode_attention_events.argtypes = so.ffd_decode_attention.argtypes + [P]
+    so.ffd_decode_attention_ex.argtypes = so.ffd_decode_attention.argtypes + [ctypes.POINTER(DecodeExtras)]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
     so.ffd_resolve_splits.argtypes = [I, I, I, I]
     for name in ("ffd_workspace_bytes", "ffd_dense_workspace_bytes"):
@@ -66,7 +72,7 @@ def lib() -> ctypes.CDLL:
         getattr(so, name).restype = SZ
     so.ffd_status_string.argtypes = [I]
     so.ffd_status_string.restype = ctypes.c_char_p
-    for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
+    for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
                  "ffd_dense_decode_attention", "ffd_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
@@ -201,13 +207,16 @@ def _attn_outputs(q, B, Hq, Lcap, want_lse, want_mask, out, lse, mask):
 def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_sink: int = 64,
                      n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
                      return_lse: bool = True, return_mask: bool = False, workspace=None,
-                     out=None, lse=None, mask=None, stage_events=None):
+                     out=None, lse=None, mask=None, stage_events=None, m_tilde=None,
+                     pseudo_max: str = "thumbnail"):
     """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested).
     The thumbnail depth is that of ``codes`` (its last dimension is 4 words per bit).
 
     ``stage_events``: optional four ``torch.cuda.Event`` objects, already recorded once (so that
     they exist), which the library records before the scan kernel, after it, after the refinement
-    kernel and after the merge."""
+    kernel and after the merge. ``m_tilde``: optional float32 ``[B, Hq]`` receiving each head's
+    pseudo-max. ``pseudo_max``: ``"thumbnail"`` (default) or ``"refined"``, the scores of the window
+    tokens the pseudo-max is taken over."""
     B, Hq, D = q.shape
     Hkv, Lcap = v.shape[1], v.shape[2]
     _need(q, "q", torch.bfloat16)
@@ -218,16 +227,22 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
                                    return_mask or mask is not None, out, lse, mask)
     if workspace is None:
         workspace = new_workspace(B, Hq, Hkv, Lcap, num_splits, q.device)
+    if pseudo_max not in PSEUDO_MAX:
+        raise ValueError(f"pseudo_max must be one of {tuple(PSEUDO_MAX)}")
+    if m_tilde is not None:
+        _need(m_tilde, "m_tilde", torch.float32, (B, Hq))
     ev = None
     if stage_events is not None:
         if len(stage_events) != 4 or any(e.cuda_event == 0 for e in stage_events):
             raise ValueError("stage_events must be four recorded torch.cuda.Event objects")
         ev = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
-    _check("ffd_decode_attention", lib().ffd_decode_attention_events(
+    extras = DecodeExtras(ctypes.cast(ev, P) if ev is not None else None, _ptr(m_tilde),
+                          PSEUDO_MAX[pseudo_max])
+    _check("ffd_decode_attention", lib().ffd_decode_attention_ex(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
         D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
         _ptr(lse), _ptr(mask), _ptr(workspace), workspace.numel() * workspace.element_size(),
-        _stream(q.device), ev))
+        _stream(q.device), ctypes.byref(extras)))
     return out, lse, mask
 
 

@@ -10,6 +10,7 @@ from oracle import ffd_oracle as O
 ATOL, RTOL = 2e-3, 1e-2
 LSE_TOL = 1e-3
 NEAR_BAND = 1e-3
+M_TILDE_TOL = 1e-4          # the pseudo-max: one fp32 rounding of an exact integer dot product (+ residual term)
 
 
 def bits_to_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:
@@ -48,15 +49,16 @@ def check_lse(name, gpu, ref, tol=LSE_TOL):
     assert not bad.any(), f"{name}: lse mismatch at {np.argwhere(bad)[:5].tolist()} gpu {gpu[bad][:5]} ref {ref[bad][:5]}"
 
 
-def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local=None, bits=2):
+def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local=None, bits=2,
+                pm_source="thumbnail", m_tilde=None):
     """Masks bit-exact outside the near-threshold band; outputs/lse against the oracle on the
-    GPU's own mask (thumbnail depth ``bits``). Returns (number of near-threshold blocks, number of
-    mismatches inside it)."""
+    GPU's own mask (thumbnail depth ``bits``, pseudo-max source ``pm_source``); the GPU's pseudo-max
+    ``m_tilde`` when given. Returns (number of near-threshold blocks, number of mismatches inside it)."""
     n_sink = case.n_sink if n_sink is None else n_sink
     n_local = case.n_local if n_local is None else n_local
     gmask = mask.cpu().numpy().astype(bool)
     ref = O.decode_batch(case.q, case.k, case.v, case.seq_lens, delta=delta, n_sink=n_sink,
-                         n_local=n_local, heads=heads, bits=bits)
+                         n_local=n_local, heads=heads, bits=bits, pm_source=pm_source)
     G = case.G
     pairs = heads if heads is not None else [(b, h) for b in range(case.B) for h in range(case.Hkv)]
     rows = [(b, h * G + i) for b, h in pairs for i in range(G)]
@@ -65,8 +67,10 @@ def compare_ffd(case, delta, out, lse, mask, *, heads=None, n_sink=None, n_local
     near = O.near_threshold(ref["sigma"][bi, hi], ref["m_tilde"][bi, hi], delta, NEAR_BAND)
     diff = gmask[bi, hi] != ref["keep"][bi, hi]
     assert not (diff & ~near).any(), f"mask mismatch outside the near-threshold band at {np.argwhere(diff & ~near)[:5].tolist()}"
+    if m_tilde is not None:
+        check_lse("m_tilde", m_tilde.cpu().numpy()[bi, hi], ref["m_tilde"][bi, hi], tol=M_TILDE_TOL)
     on_mask = O.decode_batch(case.q, case.k, case.v, case.seq_lens, delta=delta, n_sink=n_sink,
-                             n_local=n_local, keep=gmask, heads=heads, bits=bits)
+                             n_local=n_local, keep=gmask, heads=heads, bits=bits, pm_source=pm_source)
     check_close("out", bf16_to_f64(out)[bi, hi], on_mask["out"][bi, hi])
     if lse is not None:
         check_lse("lse", lse.cpu().numpy()[bi, hi], on_mask["lse"][bi, hi])

@@ -25,7 +25,7 @@ def so():
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_events",
+    for n in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
               "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes",
               "ffd_status_string"):
         assert n in names
@@ -114,3 +114,13 @@ def test_quantize_range_checks(so):
     assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 96, 2, 0, 1, None) == 2
     for bits, status in ((4, 0), (8, 0), (3, 2), (0, 1)):
         assert so.ffd_quantize_keys(None, None, None, None, 1, 8, 4096, 128, bits, 7, 7, None) == status
+
+
+def test_extras_pseudo_max_source_checked_before_launch(so):
+    from paper_2609_00097_amd import ffd
+    fake = 0x1000
+    args = [fake] * 6 + [1, 32, 8, 4096, 128, 2, 64, 5.0, 64, 256, 0, 0.0, fake, None, None, fake, 1 << 30, None]
+    bad = ffd.DecodeExtras(None, None, 7)
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(bad)) == 1
+    mis = ffd.DecodeExtras(None, fake + 2, 0)          # misaligned m_tilde
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(mis)) == 1
