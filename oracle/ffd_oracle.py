@@ -188,6 +188,18 @@ def select_blocks(sigma: np.ndarray, m_tilde: np.ndarray, delta: float) -> np.nd
     return sigma >= (m_tilde[:, None] - delta)
 
 
+def select_topk(sigma: np.ndarray, k: int) -> np.ndarray:
+    """The fixed-budget rule the paper compares against (Table 3; Fig. 1 (a)): keep, per head, the
+    ``k`` blocks with the largest block scores (all of them if there are fewer). Equal scores are
+    taken in block order, i.e. the first ``k`` of a stable sort by decreasing score."""
+    sigma = np.asarray(sigma, dtype=np.float64)
+    keep = np.zeros(sigma.shape, dtype=bool)
+    for h in range(sigma.shape[0]):
+        order = np.argsort(-sigma[h], kind="stable")
+        keep[h, order[:min(k, sigma.shape[1])]] = True
+    return keep
+
+
 # ------------------------------------------------------------------------------------------------
 # S4. Refinement with scan reuse (Alg. 1 refinement; Sec. 3.3 Eq. 4).
 # ------------------------------------------------------------------------------------------------
@@ -264,23 +276,23 @@ def lse_merge(states):
 # ------------------------------------------------------------------------------------------------
 
 def decode_group(q, K, V, L, *, delta, n_sink, n_local, block, alpha, keep=None, bits=2,
-                 pm_source="thumbnail"):
+                 pm_source="thumbnail", topk=0):
     """FFD decode for the ``G`` query heads ``q [G, d]`` sharing keys ``K [Lcap, d]``, values ``V``.
 
     Follows Alg. 1 in order: quantize, pseudo-max, top-delta selection, refinement, softmax . V.
     When ``keep`` (bool ``[G, nblk]``) is given, attention runs on that mask instead of the
     oracle's own selection (used to compare outputs given the GPU's mask). ``bits`` is the
     thumbnail depth (App. C); ``pm_source`` the scores the pseudo-max is taken over
-    (:func:`window_scores`).
+    (:func:`window_scores`); ``topk > 0`` replaces the top-delta rule by :func:`select_topk`.
     """
     codes, M, resid = quantize_keys(K[:L], bits)
     return decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=n_sink,
                                   n_local=n_local, block=block, alpha=alpha, keep=keep, bits=bits,
-                                  pm_source=pm_source, K=K)
+                                  pm_source=pm_source, K=K, topk=topk)
 
 
 def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, block, alpha,
-                           keep=None, bits=2, pm_source="thumbnail", K=None):
+                           keep=None, bits=2, pm_source="thumbnail", K=None, topk=0):
     """The decode step of :func:`decode_group` given the already quantized keys (Alg. 1 from the
     pseudo-max on; the quantization happens when the cache is written, Fig. 2). ``K`` (the exact
     keys) is needed only for ``pm_source="exact"``."""
@@ -288,7 +300,7 @@ def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, 
     z_all = refined_logits(q, codes, M, resid, alpha, bits)
     m_tilde = pseudo_max(window_scores(pm_source, s_hat, z_all, q, K, L, alpha), L, n_sink, n_local)
     sigma = block_scores(s_hat, L, block)
-    own_keep = select_blocks(sigma, m_tilde, delta)
+    own_keep = select_topk(sigma, topk) if topk > 0 else select_blocks(sigma, m_tilde, delta)
     use = own_keep if keep is None else np.asarray(keep, dtype=bool)[:, :sigma.shape[1]]
     outs, lses = [], []
     for h in range(q.shape[0]):
@@ -301,13 +313,14 @@ def decode_group_quantized(q, codes, M, resid, V, L, *, delta, n_sink, n_local, 
 
 
 def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, block=64,
-                 softmax_scale=None, keep=None, heads=None, bits=2, pm_source="thumbnail"):
+                 softmax_scale=None, keep=None, heads=None, bits=2, pm_source="thumbnail", topk=0):
     """FFD decode for a batch. Inputs are bf16 bit patterns ``q [B,Hq,d]``, ``k, v [B,Hkv,Lcap,d]``.
 
     Returns float64 ``out [B,Hq,d]``, ``lse [B,Hq]``, the per-head block mask ``keep [B,Hq,nblk]``
     (blocks at or beyond a sequence's end are False), ``sigma`` and ``m_tilde``.
     ``heads`` optionally restricts work to a list of ``(b, kvh)`` pairs (others left as NaN);
-    ``bits`` is the thumbnail depth (App. C), ``pm_source`` the pseudo-max's scores.
+    ``bits`` is the thumbnail depth (App. C), ``pm_source`` the pseudo-max's scores, ``topk > 0``
+    the fixed-budget rule instead of top-delta.
     """
     B, Hq, d = q_bits.shape
     Hkv, Lcap = k_bits.shape[1], k_bits.shape[2]
@@ -333,7 +346,7 @@ def decode_batch(q_bits, k_bits, v_bits, seq_lens, *, delta, n_sink, n_local, bl
         V = bf16_to_f64(v_bits[b, h, :L])
         kb = None if keep is None else np.asarray(keep[b, sl], dtype=bool)
         r = decode_group(q, K, V, L, delta=delta, n_sink=n_sink, n_local=n_local, block=block,
-                         alpha=alpha, keep=kb, bits=bits, pm_source=pm_source)
+                         alpha=alpha, keep=kb, bits=bits, pm_source=pm_source, topk=topk)
         nb = r["sigma"].shape[1]
         out[b, sl] = r["out"]
         lse[b, sl] = r["lse"]
