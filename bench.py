@@ -18,6 +18,8 @@ under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep. ``de
 same step with 4- and 8-bit thumbnails (the 4+8 and 8+8 depths of App. C) beside the 2+8 headline.
 ``fidelity`` gives Sec. 5.1's recall (cosine with the dense output) and LSE error and Sec. 5.2's
 pseudo-max gap m - m~ for each delta, with the pseudo-max over thumbnail or refined window scores.
+``selection_rule`` times the fixed-budget (top-k) rule with k matched to top-delta's mean keep
+ratio (Table 3's selection-rule overhead comparison), on the same scan and refinement.
 """
 from __future__ import annotations
 
@@ -223,18 +225,19 @@ class Runner:
     def flush(self):
         self.torch.sum(self.flush_buf)
 
-    def ffd_step(self, delta, events=None, mask=None):
+    def ffd_step(self, delta, events=None, mask=None, top_k=0):
         c = self.case
         self.ffd.decode_attention(self.q, *self.qk, self.v, self.lens, delta=delta, n_sink=c.n_sink,
                                   n_local=c.n_local, num_splits=self.splits, workspace=self.ws,
-                                  out=self.out, lse=self.lse, mask=mask, stage_events=events)
+                                  out=self.out, lse=self.lse, mask=mask, stage_events=events,
+                                  top_k=top_k)
 
     def dense_step(self):
         self.ffd.dense_decode_attention(self.q, self.k, self.v, self.lens, num_splits=self.splits,
                                         workspace=self.dws, out=self.out, lse=self.lse)
 
-    def mask_for(self, delta):
-        self.ffd_step(delta, mask=self.mask)
+    def mask_for(self, delta, top_k=0):
+        self.ffd_step(delta, mask=self.mask, top_k=top_k)
         self.torch.cuda.synchronize()
         return self.mask.cpu().numpy().astype(bool)
 
@@ -319,6 +322,35 @@ def depth_sweep(r, delta, depths, steps, dense_us):
         torch.cuda.empty_cache()
     r.qk = saved
     return out
+
+
+def selection_rule(r, delta, keep, steps, dense_us, stage_us):
+    """Table 3's comparison on one scan and refinement: the fixed-budget rule with k = top-delta's
+    mean kept blocks per head, timed like the headline, with its own kernels' event times."""
+    c = r.case
+    nb = np.array([-(-int(L) // 64) for L in c.seq_lens])
+    kept = sum(int(keep[b, :, :nb[b]].sum()) for b in range(c.B))
+    k = max(1, int(round(kept / float(c.B * c.Hq))))
+    kk = r.mask_for(delta, top_k=k)
+    bk = algorithmic_bytes(c, kk, r.S)
+    ms, _ = r.time(lambda: r.ffd_step(delta, top_k=k), steps, 5)
+    _, _, st = r.time(lambda ev: r.ffd_step(delta, events=ev, top_k=k), steps, 3, stages=True)
+    su = st.mean(axis=0) * 1e3
+    us = float(ms.mean() * 1e3)
+    ratio = lambda m: float(np.mean(np.concatenate([m[b, :, :nb[b]].ravel() for b in range(c.B)])))
+    return {"k": k, "top_k_us": round(us, 2),
+            "top_k_keep_head_blocks": round(ratio(kk), 5),
+            "top_delta_keep_head_blocks": round(ratio(keep), 5),
+            "top_k_keep_union_tokens": round(bk["gather_tokens"] / float(c.seq_lens.sum() * c.Hkv), 5),
+            "top_k_stages_us": {"scan_and_select": round(float(su[0]), 2), "refine": round(float(su[1]), 2),
+                                "merge": round(float(su[2]), 2)},
+            "top_delta_stages_us": {"scan_and_select": round(float(stage_us[0]), 2),
+                                    "refine": round(float(stage_us[1]), 2), "merge": round(float(stage_us[2]), 2)},
+            "top_k_speedup_vs_dense": round(dense_us / us, 2),
+            "what": "top-k keeps per head the k blocks with the largest thumbnail block scores (scan, "
+                    "then a per-(sequence, KV head) radix-select kernel, then the refinement recomputing "
+                    "the kept blocks' thumbnail scores); k = top-delta's mean kept blocks per head at "
+                    "this delta; stage times from library events in separate steps"}
 
 
 def exact_max(r):
@@ -473,6 +505,8 @@ def main():
                          "keep_head_blocks": round(float(kd.mean()), 5),
                          "speedup_vs_dense": round(dense_us / su, 2)}
 
+    stage_us = stage_ms.mean(axis=0) * 1e3
+    selection = selection_rule(r, args.delta, keep, 30, dense_us, stage_us)
     ceiling = stream_ceiling(r)
     depths = depth_sweep(r, args.delta, [int(x) for x in args.depths.split(",") if x.strip()],
                          20, dense_us)
@@ -480,7 +514,6 @@ def main():
     loop = decode_loop(r, args.delta, min(args.steps, 60), 10)      # writes the caches: run last
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
-    stage_us = stage_ms.mean(axis=0) * 1e3
     stage_bytes = {"ffd_scan_kernel": nbytes["scan"] + case.B * case.Hq * 2 * case.D,
                    "ffd_refine_kernel": nbytes["gather"],
                    "lse_merge_kernel": nbytes["partials"] // 2 + case.B * case.Hq * (2 * case.D + 4)}
@@ -527,6 +560,7 @@ def main():
         "depth_sweep": {"2+8": {"us": round(eager_us, 2), "scan_us": round(float(stage_us[0]), 2),
                                 "refine_us": round(float(stage_us[1]), 2),
                                 "merge_us": round(float(stage_us[2]), 2)}, **depths},
+        "selection_rule": selection,
         "stream_ceiling": ceiling,
         "fidelity": fid,
         "decode_loop": loop,

@@ -163,11 +163,20 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
  *   pseudo_max    FFD_PSEUDO_MAX_THUMBNAIL or FFD_PSEUDO_MAX_REFINED (other values:
  *                 FFD_ERR_INVALID_ARGUMENT). The refined source reads the window blocks' residuals
  *                 as well; the selection still compares thumbnail block scores with m~ - delta.
+ *   top_k         0: the top-delta rule. k > 0: the fixed-budget rule the paper compares top-delta
+ *                 with (Sec. 1 and Fig. 1 (a); Table 3's selection-rule overhead): each head keeps
+ *                 the min(k, blocks) blocks with the largest thumbnail block scores, equal scores
+ *                 taken in block order; delta, n_sink, n_local and pseudo_max are then unused and
+ *                 m_tilde must be NULL. The call then launches four kernels: the scan (writing every
+ *                 block score), a per-(sequence, KV head) selection kernel, the refinement
+ *                 (recomputing the kept blocks' thumbnail scores from the codes) and the merge; the
+ *                 second stage event follows the selection kernel. Negative: FFD_ERR_INVALID_ARGUMENT.
  */
 typedef struct ffd_decode_extras {
     hipEvent_t* stage_events;
     float* m_tilde;
     int pseudo_max;
+    int top_k;
 } ffd_decode_extras;
 
 /*

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libffd.so")
-SOURCES = ["ffd_api.hip", "ffd_decode.hip", "ffd_dense.hip", "ffd_merge.hip", "ffd_quantize.hip"]
+SOURCES = ["ffd_api.hip", "ffd_decode.hip", "ffd_dense.hip", "ffd_merge.hip", "ffd_quantize.hip",
+           "ffd_topk.hip"]
 ARCH = os.environ.get("FFD_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [

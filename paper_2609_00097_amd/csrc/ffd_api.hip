@@ -132,25 +132,36 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
     return FFD_OK;
 }
 
-// The scan kernel for this depth, head tiling and pseudo-max source.
+// The scan kernel for this depth, head tiling and selection mode (ScanMode).
 template <int NT, int BITS>
-void launch_scan_nt(bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
-    if (refined_pm)
-        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, true>), grid, dim3(kThreads), 0, stream, sa);
+void launch_scan_nt(int mode, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (mode == kSelRefinedPM)
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelRefinedPM>), grid, dim3(kThreads), 0, stream, sa);
+    else if (mode == kSelTopK)
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelTopK>), grid, dim3(kThreads), 0, stream, sa);
     else
-        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, false>), grid, dim3(kThreads), 0, stream, sa);
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelThumbnailPM>), grid, dim3(kThreads), 0, stream, sa);
 }
 
 template <int BITS>
-void launch_scan_bits(int nt, bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
-    if (nt == 1) launch_scan_nt<1, BITS>(refined_pm, grid, stream, sa);
-    else launch_scan_nt<2, BITS>(refined_pm, grid, stream, sa);
+void launch_scan_bits(int nt, int mode, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (nt == 1) launch_scan_nt<1, BITS>(mode, grid, stream, sa);
+    else launch_scan_nt<2, BITS>(mode, grid, stream, sa);
 }
 
-void launch_scan(int bits, int nt, bool refined_pm, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
-    if (bits == 2) launch_scan_bits<2>(nt, refined_pm, grid, stream, sa);
-    else if (bits == 4) launch_scan_bits<4>(nt, refined_pm, grid, stream, sa);
-    else launch_scan_bits<8>(nt, refined_pm, grid, stream, sa);
+void launch_scan(int bits, int nt, int mode, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
+    if (bits == 2) launch_scan_bits<2>(nt, mode, grid, stream, sa);
+    else if (bits == 4) launch_scan_bits<4>(nt, mode, grid, stream, sa);
+    else launch_scan_bits<8>(nt, mode, grid, stream, sa);
+}
+
+// The refinement kernel: scan scores from the workspace (rbits = 0) or recomputed from rbits-bit codes.
+template <int NT>
+void launch_refine_nt(int rbits, dim3 grid, hipStream_t stream, const RefineArgs& ra) {
+    if (rbits == 0) hipLaunchKernelGGL((ffd_refine_kernel<NT, 0>), grid, dim3(kThreads), 0, stream, ra);
+    else if (rbits == 2) hipLaunchKernelGGL((ffd_refine_kernel<NT, 2>), grid, dim3(kThreads), 0, stream, ra);
+    else if (rbits == 4) hipLaunchKernelGGL((ffd_refine_kernel<NT, 4>), grid, dim3(kThreads), 0, stream, ra);
+    else hipLaunchKernelGGL((ffd_refine_kernel<NT, 8>), grid, dim3(kThreads), 0, stream, ra);
 }
 
 }  // namespace
@@ -243,8 +254,10 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     hipEvent_t* stage_events = extras ? extras->stage_events : nullptr;
     float* m_tilde = extras ? extras->m_tilde : nullptr;
     const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
+    const int top_k = extras ? extras->top_k : 0;
     if (pm_source != FFD_PSEUDO_MAX_THUMBNAIL && pm_source != FFD_PSEUDO_MAX_REFINED)
         return FFD_ERR_INVALID_ARGUMENT;
+    if (top_k < 0 || (top_k > 0 && m_tilde)) return FFD_ERR_INVALID_ARGUMENT;
     if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
     if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
     int S = 0;
@@ -273,26 +286,41 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     const int S1 = scan_splits(B, Hkv, Lcap);
     const int npairs = B * Hkv;
     const int Wr = S * npairs;
+    // top-k: the block scores [P, C, G] take the place of the kept blocks' scan scores (which the
+    // refinement then recomputes from the codes)
+    float* sigma = shat;
     ScanArgs sa{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
                 static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid), seq_lens, lists,
-                counts, shat, block_mask, m_tilde, Hq, Hkv, Lcap, G, S1, delta, scale, n_sink, n_local};
-    RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_absmax),
+                counts, shat, sigma, block_mask, m_tilde, Hq, Hkv, Lcap, G, S1, delta, scale, n_sink, n_local};
+    RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
+                  static_cast<const uint16_t*>(k_absmax),
                   static_cast<const int8_t*>(k_resid), static_cast<const uint16_t*>(v), seq_lens, lists,
                   counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale,
                   thumb_top_level(thumb_bits)};
+    TopkArgs ta{sigma, seq_lens, lists, counts, block_mask, Hq, Hkv, Lcap, S1, top_k};
     const dim3 scan_grid((unsigned)S1, (unsigned)Hkv, (unsigned)B);
     const dim3 refine_grid((unsigned)(Wr + npairs));
     auto mark = [&](int i) {
         return stage_events && hipEventRecord(stage_events[i], stream) != hipSuccess ? FFD_ERR_HIP : FFD_OK;
     };
 
+    const int mode = top_k > 0 ? kSelTopK : (pm_source == FFD_PSEUDO_MAX_REFINED ? kSelRefinedPM : kSelThumbnailPM);
     if ((st = mark(0)) != FFD_OK) return st;
-    launch_scan(thumb_bits, G <= 4 ? 1 : 2, pm_source == FFD_PSEUDO_MAX_REFINED, scan_grid, stream, sa);
-    if ((st = launch_status()) != FFD_OK || (st = mark(1)) != FFD_OK) return st;
-    if (G <= 4)
-        hipLaunchKernelGGL(ffd_refine_kernel<1>, refine_grid, dim3(kThreads), 0, stream, ra);
-    else
-        hipLaunchKernelGGL(ffd_refine_kernel<2>, refine_grid, dim3(kThreads), 0, stream, ra);
+    launch_scan(thumb_bits, G <= 4 ? 1 : 2, mode, scan_grid, stream, sa);
+    if ((st = launch_status()) != FFD_OK) return st;
+    if (top_k > 0) {
+        const dim3 grid((unsigned)npairs);
+        const dim3 block(kTopkSelectThreads);
+        if (G == 1) hipLaunchKernelGGL(ffd_topk_select_kernel<1>, grid, block, 0, stream, ta);
+        else if (G == 2) hipLaunchKernelGGL(ffd_topk_select_kernel<2>, grid, block, 0, stream, ta);
+        else if (G == 4) hipLaunchKernelGGL(ffd_topk_select_kernel<4>, grid, block, 0, stream, ta);
+        else hipLaunchKernelGGL(ffd_topk_select_kernel<8>, grid, block, 0, stream, ta);
+        if ((st = launch_status()) != FFD_OK) return st;
+    }
+    if ((st = mark(1)) != FFD_OK) return st;
+    const int rbits = top_k > 0 ? thumb_bits : 0;
+    if (G <= 4) launch_refine_nt<1>(rbits, refine_grid, stream, ra);
+    else launch_refine_nt<2>(rbits, refine_grid, stream, ra);
     if ((st = launch_status()) != FFD_OK || (st = mark(2)) != FFD_OK) return st;
     hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, part_m, part_l,
                        part_acc, 0, table, G, static_cast<uint16_t*>(out), lse);

@@ -175,8 +175,36 @@ __device__ __forceinline__ BlockScan<BITS> load_block_scan(const uint32_t* __res
     return r;
 }
 
+// Thumbnail scores of one 16-token tile for this lane's head(s) and token n: tw holds the lane's b
+// words of the tile (64-dim chunk 0, then chunk 1), M the token's absmax; -inf for a token past L.
+template <int NT, int BITS>
+__device__ __forceinline__ void tile_scores(const uint32_t* tw, float M, bool valid, const HeadConsts<NT>& hc,
+                                            float (&sc)[NT]) {
+    const v4i b0 = expand_codes<BITS>(tw);
+    const v4i b1 = expand_codes<BITS>(tw + BITS / 2);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        v4i acc = {0, 0, 0, 0};
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], b0, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], b1, acc, 0, 0, 0);
+        float Tf;
+        if constexpr (BITS == 2) {
+            // |sum_d Q_d (2 c_d - 3)| <= 3 * 128 * 2^22 < 2^31: exact modulo 2^32
+            const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
+            Tf = (float)(int)(2u * s - 3u * (uint32_t)hc.sumq[t]);
+        } else {
+            const long long s = (long long)acc.x + ((long long)acc.y << 8) + ((long long)acc.z << 16);
+            // 8-bit codes are the bytes c - 128, and 2c - 255 = 2 (c - 128) + 1
+            const long long T = BITS == 8 ? 2 * s + hc.sumq[t]
+                                          : 2 * s - (long long)((1 << BITS) - 1) * hc.sumq[t];
+            Tf = (float)T;
+        }
+        sc[t] = valid ? Tf * (M * hc.kap[t]) : -INFINITY;
+    }
+}
+
 // Thumbnail scores of block j for this lane's head(s) and tokens 64j + 16*T4 + n; -inf past L.
-// Lane words of tile T4, chunk cc start at word (2 T4 + cc) b/2 (the storage layout of ffd.h).
+// Lane words of tile T4 are words T4*b .. T4*b + b - 1 (the storage layout of ffd.h).
 template <int NT, int BITS>
 __device__ __forceinline__ void block_scores(const BlockScan<BITS>& ld, int j, int lane, int L,
                                              const HeadConsts<NT>& hc, float (&sc)[NT][4]) {
@@ -190,28 +218,10 @@ __device__ __forceinline__ void block_scores(const BlockScan<BITS>& ld, int j, i
     }
 #pragma unroll
     for (int T4 = 0; T4 < 4; ++T4) {
-        const v4i b0 = expand_codes<BITS>(&words[(2 * T4 + 0) * (BITS / 2)]);
-        const v4i b1 = expand_codes<BITS>(&words[(2 * T4 + 1) * (BITS / 2)]);
-        const bool valid = 64 * j + 16 * T4 + n < L;
+        float st[NT];
+        tile_scores<NT, BITS>(&words[T4 * BITS], M[T4], 64 * j + 16 * T4 + n < L, hc, st);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            v4i acc = {0, 0, 0, 0};
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], b0, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], b1, acc, 0, 0, 0);
-            float Tf;
-            if constexpr (BITS == 2) {
-                // |sum_d Q_d (2 c_d - 3)| <= 3 * 128 * 2^22 < 2^31: exact modulo 2^32
-                const uint32_t s = (uint32_t)acc.x + ((uint32_t)acc.y << 8) + ((uint32_t)acc.z << 16);
-                Tf = (float)(int)(2u * s - 3u * (uint32_t)hc.sumq[t]);
-            } else {
-                const long long s = (long long)acc.x + ((long long)acc.y << 8) + ((long long)acc.z << 16);
-                // 8-bit codes are the bytes c - 128, and 2c - 255 = 2 (c - 128) + 1
-                const long long T = BITS == 8 ? 2 * s + hc.sumq[t]
-                                              : 2 * s - (long long)((1 << BITS) - 1) * hc.sumq[t];
-                Tf = (float)T;
-            }
-            sc[t][T4] = valid ? Tf * (M[T4] * hc.kap[t]) : -INFINITY;
-        }
+        for (int t = 0; t < NT; ++t) sc[t][T4] = st[t];
     }
 }
 
@@ -226,56 +236,50 @@ struct ScanLds {
 // ---- refinement helpers ---------------------------------------------------------------------
 
 // One wave's loads for one 16-token tile of a kept block: int8 residual, its lane's value dwords,
-// the stored scan scores of its heads and the token's absmax.
-template <int NT>
+// the token's absmax, and either the stored scan scores of its heads (RBITS = 0) or the lane's
+// RBITS code words of the tile, from which the scan scores are recomputed.
+template <int NT, int RBITS>
 struct RefineTile {
     v4i r0, r1;
     VTile vt;
-    float sc[NT];
+    float sc[RBITS == 0 ? NT : 1];
+    uint32_t cw[RBITS == 0 ? 1 : RBITS];
     uint32_t m;       // absmax bf16 bits in the low half
 };
 
-template <int NT>
-__device__ __forceinline__ RefineTile<NT> load_refine_tile(const int8_t* __restrict__ resid_bh,
-                                                           const uint16_t* __restrict__ v_bh,
-                                                           const float* __restrict__ shat_bh,
-                                                           const uint16_t* __restrict__ absmax_bh,
-                                                           int j, int T4, int lane, int last_row) {
-    RefineTile<NT> r;
+template <int NT, int RBITS>
+__device__ __forceinline__ RefineTile<NT, RBITS> load_refine_tile(const int8_t* __restrict__ resid_bh,
+                                                                  const uint16_t* __restrict__ v_bh,
+                                                                  const float* __restrict__ shat_bh,
+                                                                  const uint32_t* __restrict__ codes_bh,
+                                                                  const uint16_t* __restrict__ absmax_bh,
+                                                                  int j, int T4, int lane, int last_row) {
+    RefineTile<NT, RBITS> r;
     const int tile = 4 * j + T4;
     const v4i* rp = reinterpret_cast<const v4i*>(resid_bh) + (size_t)tile * 128 + lane;
     r.r0 = rp[0];
     r.r1 = rp[64];
     r.vt = load_vtile(v_bh, 16 * tile, last_row, lane);
-    const float* sp = shat_bh + (size_t)tile * (NT * 64) + lane;
+    if constexpr (RBITS == 0) {
+        const float* sp = shat_bh + (size_t)tile * (NT * 64) + lane;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) r.sc[t] = sp[64 * t];
+        for (int t = 0; t < NT; ++t) r.sc[t] = sp[64 * t];
+    } else {
+        // the lane's 4b words of block j; tile T4 is words T4*b .. T4*b + b - 1
+        const uint32_t* cp = codes_bh + ((size_t)j * 64 + lane) * (4 * RBITS) + T4 * RBITS;
+        if constexpr (RBITS == 2) {
+            const uint2 w = *reinterpret_cast<const uint2*>(cp);
+            r.cw[0] = w.x; r.cw[1] = w.y;
+        } else {
+#pragma unroll
+            for (int i = 0; i < RBITS / 4; ++i) {
+                const uint4 w = reinterpret_cast<const uint4*>(cp)[i];
+                r.cw[4 * i] = w.x; r.cw[4 * i + 1] = w.y; r.cw[4 * i + 2] = w.z; r.cw[4 * i + 3] = w.w;
+            }
+        }
+    }
     r.m = absmax_bh[(size_t)j * 64 + (lane & 15) * 4 + T4];
     return r;
-}
-
-// Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum. One
-// barrier: consecutive calls must alternate between the two halves of wsum[2][kWaves] (a wave
-// reaching call k + 2 has passed call k + 1's barrier, so every wave has read call k's half).
-__device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int incl = x;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o);
-        if (lane >= o) incl += y;
-    }
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    int before = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        const int s = wsum[w];
-        before += w < wave ? s : 0;
-        tot += s;
-    }
-    *total = tot;
-    return before + incl - x;
 }
 
 constexpr int kPairChunk = 4 * kThreads;     // KV groups allocated per pass (4 per thread)
@@ -338,12 +342,13 @@ __device__ __forceinline__ void add_residual_term(const int8_t* __restrict__ res
 }
 
 // Workgroups per CU: the 8-bit blocks and the refined pseudo-max's residual tiles need more registers.
-template <int NT, int BITS, bool REFINED_PM> constexpr int scan_occupancy() {
-    return BITS == 8 ? 2 : (REFINED_PM ? (NT == 1 ? 3 : 2) : 4);
+template <int NT, int BITS, int MODE> constexpr int scan_occupancy() {
+    return BITS == 8 ? 2 : (MODE == kSelRefinedPM ? (NT == 1 ? 3 : 2) : 4);
 }
 
-template <int NT, int BITS, bool REFINED_PM>
-__global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>())) void ffd_scan_kernel(ScanArgs a) {
+template <int NT, int BITS, int MODE>
+__global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void ffd_scan_kernel(ScanArgs a) {
+    constexpr bool kTopK = MODE == kSelTopK;
     constexpr int kRing = scan_ring<BITS>();
     constexpr int kPMW = scan_pmw<BITS>();
     __shared__ ScanLds<NT> sm;
@@ -357,9 +362,11 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
     const int nblk_cap = a.Lcap / kBlock;
     const int bps = (nblk + a.S1 - 1) / a.S1;
     const int jb = min(s * bps, nblk), je = min(jb + bps, nblk);
-    if (jb >= je && !a.mask) {                  // nothing to scan (short sequence), nothing to clear
-        if (tid == 0) a.counts[bh * a.S1 + s] = 0;
-        if (a.m_tilde && s == 0 && tid < G) a.m_tilde[(size_t)b * a.Hq + hq0 + tid] = -INFINITY;   // L = 0
+    if (jb >= je && (kTopK || !a.mask)) {       // nothing to scan (short sequence), nothing to clear
+        if constexpr (!kTopK) {
+            if (tid == 0) a.counts[bh * a.S1 + s] = 0;
+            if (a.m_tilde && s == 0 && tid < G) a.m_tilde[(size_t)b * a.Hq + hq0 + tid] = -INFINITY;   // L = 0
+        }
         return;
     }
 
@@ -386,10 +393,12 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
     const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
     BlockScan<BITS> win[kPMW];
+    if constexpr (!kTopK) {
 #pragma unroll
-    for (int i = 0; i < kPMW; ++i)
-        win[i] = load_block_scan<BITS>(codes_bh, absmax_bh,
-                                       min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
+        for (int i = 0; i < kPMW; ++i)
+            win[i] = load_block_scan<BITS>(codes_bh, absmax_bh,
+                                           min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
+    }
     BlockScan<BITS> ring[kRing];
 #pragma unroll
     for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
@@ -398,47 +407,52 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
     build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
 
     // ---- pseudo-max over sink and local windows (Eq. 3) ----------------------------------
-    float pm[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) pm[t] = -INFINITY;
-    for (int base = 0; base < npm; base += kWaves * kPMW) {
-        if (base > 0) {
-#pragma unroll
-            for (int i = 0; i < kPMW; ++i)
-                win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, pm_block(min(base + kWaves * i + wave, npm - 1)), lane);
-        }
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i) {
-            const int idx = base + kWaves * i + wave;
-            const int j = pm_block(min(idx, npm - 1));
-            float sc[NT][4];
-            block_scores<NT, BITS>(win[i], j, lane, L, hc, sc);
-            if constexpr (REFINED_PM)
-                add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win[i].mm, j, lane, hc, sc);
-#pragma unroll
-            for (int T4 = 0; T4 < 4; ++T4) {
-                const int tok = 64 * j + 16 * T4 + n;
-                const bool in_win = idx < npm && tok < L && (tok < sink_end || tok >= loc_beg);
-#pragma unroll
-                for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
-            }
-        }
-    }
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        pm[t] = row16_max(pm[t]);
-        if (n == 0) sm.pm[wave][4 * t + g] = pm[t];
-    }
-    __syncthreads();
+    // (not needed by the top-k rule, which compares block scores with each other)
     float thr[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        float m = -INFINITY;
+    for (int t = 0; t < NT; ++t) thr[t] = -INFINITY;
+    if constexpr (!kTopK) {
+        float pm[NT];
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][4 * t + g]);
-        thr[t] = m - a.delta;                      // -inf when both windows are empty
-        if (a.m_tilde && s == 0 && wave == 0 && n == 0 && hc.live[t])
-            a.m_tilde[(size_t)b * a.Hq + hq0 + 4 * t + g] = m;
+        for (int t = 0; t < NT; ++t) pm[t] = -INFINITY;
+        for (int base = 0; base < npm; base += kWaves * kPMW) {
+            if (base > 0) {
+#pragma unroll
+                for (int i = 0; i < kPMW; ++i)
+                    win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, pm_block(min(base + kWaves * i + wave, npm - 1)), lane);
+            }
+#pragma unroll
+            for (int i = 0; i < kPMW; ++i) {
+                const int idx = base + kWaves * i + wave;
+                const int j = pm_block(min(idx, npm - 1));
+                float sc[NT][4];
+                block_scores<NT, BITS>(win[i], j, lane, L, hc, sc);
+                if constexpr (MODE == kSelRefinedPM)
+                    add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win[i].mm, j, lane, hc, sc);
+#pragma unroll
+                for (int T4 = 0; T4 < 4; ++T4) {
+                    const int tok = 64 * j + 16 * T4 + n;
+                    const bool in_win = idx < npm && tok < L && (tok < sink_end || tok >= loc_beg);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
+                }
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            pm[t] = row16_max(pm[t]);
+            if (n == 0) sm.pm[wave][4 * t + g] = pm[t];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            float m = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][4 * t + g]);
+            thr[t] = m - a.delta;                      // -inf when both windows are empty
+            if (a.m_tilde && s == 0 && wave == 0 && n == 0 && hc.live[t])
+                a.m_tilde[(size_t)b * a.Hq + hq0 + 4 * t + g] = m;
+        }
     }
 
     // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
@@ -446,6 +460,16 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
     auto decide = [&](const BlockScan<BITS>& blk, int j) {
         float sc[NT][4];
         block_scores<NT, BITS>(blk, j, lane, L, hc, sc);
+        if constexpr (kTopK) {
+            float* sigma_bh = a.sigma + bh * (size_t)nblk_cap * G;
+            // sigma only: + 0 turns a -0 score (a zero key) into +0, so equal scores compare equal
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3]))) + 0.f;
+                if (n == 0 && hc.live[t]) sigma_bh[(size_t)j * G + 4 * t + g] = sig;
+            }
+            return;
+        }
         uint32_t bits = 0;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -483,6 +507,8 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
     for (int r = 0; r < kRing; ++r)
         if (i0 + r < nbw) decide(ring[r], jw0 + i0 + r);
 
+    if constexpr (kTopK) return;
+
     // ---- this workgroup's kept list, in block order, and its length ------------------------
     if (lane == 0) sm.nkept[wave] = nkept;
     __syncthreads();
@@ -511,7 +537,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, REFINED_PM>()))
 // group refines its kept blocks of rank [p n_x / W_x, (p + 1) n_x / W_x). Workgroups past the last
 // group's exit.
 // ================================================================================================
-template <int NT>
+template <int NT, int RBITS>
 __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(RefineArgs a) {
     __shared__ RefineLds<NT> sm;
     const int wg = blockIdx.x;
@@ -635,6 +661,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const int8_t* resid_bh = a.resid + bh * (size_t)a.Lcap * kD;
     const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
     const float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
+    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * (RBITS == 0 ? 2 : RBITS));
     const uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap;
 
     uint32_t qw[NT];
@@ -666,17 +693,24 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     TileP<NT>& tp = sm.tp[wave];
 
     // refine (Eq. 4) and attend tile `wave` of one kept block
-    auto attend = [&](const RefineTile<NT>& rt, uint32_t bits) {
+    auto attend = [&](const RefineTile<NT, RBITS>& rt, int j, uint32_t bits) {
         float z[NT];
         bool keep[NT];
         const float Mt = bf16_to_f32((uint16_t)rt.m);
+        float shat[NT];
+        if constexpr (RBITS == 0) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) shat[t] = rt.sc[t];
+        } else {
+            tile_scores<NT, RBITS>(rt.cw, Mt, 64 * j + 16 * wave + n < L, hc, shat);
+        }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             v4i acc = {0, 0, 0, 0};
             acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], rt.r0, acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], rt.r1, acc, 0, 0, 0);
             const float R = fmaf(65536.f, (float)acc.z, fmaf(256.f, (float)acc.y, (float)acc.x));
-            const float sct = rt.sc[t];
+            const float sct = shat[t];
             z[t] = sct == -INFINITY ? -INFINITY : fmaf(R, Mt * hc.kap2[t], sct);
             keep[t] = (bits >> (4 * t + g)) & 1u;
         }
@@ -704,19 +738,20 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         }
         __syncthreads();
         auto block_of = [&](int i) { return (int)(sm.u.list[min(i, m - 1)] & 0xffffffu); };
-        RefineTile<NT> ring[kRefineRing];
+        RefineTile<NT, RBITS> ring[kRefineRing];
 #pragma unroll
         for (int r = 0; r < kRefineRing; ++r)
-            ring[r] = load_refine_tile<NT>(resid_bh, v_bh, shat_bh, absmax_bh, block_of(r), wave, lane, last_row);
+            ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, shat_bh, codes_bh, absmax_bh, block_of(r), wave,
+                                                  lane, last_row);
         // the refill of the last round re-reads the share's last tile (clamped): it is still
         // cached, and a conditional refill would cost more registers than it saves
         for (int i0 = 0; i0 < m; i0 += kRefineRing) {
 #pragma unroll
             for (int r = 0; r < kRefineRing; ++r) {
                 const int i = i0 + r;
-                if (i < m) attend(ring[r], sm.u.list[i] >> 24);
-                ring[r] = load_refine_tile<NT>(resid_bh, v_bh, shat_bh, absmax_bh,
-                                               block_of(i + kRefineRing), wave, lane, last_row);
+                if (i < m) attend(ring[r], (int)(sm.u.list[i] & 0xffffffu), sm.u.list[i] >> 24);
+                ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, shat_bh, codes_bh, absmax_bh,
+                                                      block_of(i + kRefineRing), wave, lane, last_row);
             }
         }
         __syncthreads();                // the list is rewritten by the next chunk / the epilogue
@@ -726,19 +761,31 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                        a.part_l, a.part_acc);
 }
 
-template __global__ void ffd_scan_kernel<1, 2, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 2, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 4, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 4, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 8, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 8, false>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 2, true>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 2, true>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 4, true>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 4, true>(ScanArgs);
-template __global__ void ffd_scan_kernel<1, 8, true>(ScanArgs);
-template __global__ void ffd_scan_kernel<2, 8, true>(ScanArgs);
-template __global__ void ffd_refine_kernel<1>(RefineArgs);
-template __global__ void ffd_refine_kernel<2>(RefineArgs);
+template __global__ void ffd_scan_kernel<1, 2, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8, kSelThumbnailPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 2, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8, kSelRefinedPM>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 2, kSelTopK>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 2, kSelTopK>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 4, kSelTopK>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 4, kSelTopK>(ScanArgs);
+template __global__ void ffd_scan_kernel<1, 8, kSelTopK>(ScanArgs);
+template __global__ void ffd_scan_kernel<2, 8, kSelTopK>(ScanArgs);
+template __global__ void ffd_refine_kernel<1, 0>(RefineArgs);
+template __global__ void ffd_refine_kernel<2, 0>(RefineArgs);
+template __global__ void ffd_refine_kernel<1, 2>(RefineArgs);
+template __global__ void ffd_refine_kernel<2, 2>(RefineArgs);
+template __global__ void ffd_refine_kernel<1, 4>(RefineArgs);
+template __global__ void ffd_refine_kernel<2, 4>(RefineArgs);
+template __global__ void ffd_refine_kernel<1, 8>(RefineArgs);
+template __global__ void ffd_refine_kernel<2, 8>(RefineArgs);
 
 }  // namespace ffd

@@ -69,6 +69,30 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum. One
+// barrier: consecutive calls must alternate between the two halves of wsum[2][kWaves] (a wave
+// reaching call k + 2 has passed call k + 1's barrier, so every wave has read call k's half).
+__device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int incl = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int s = wsum[w];
+        before += w < wave ? s : 0;
+        tot += s;
+    }
+    *total = tot;
+    return before + incl - x;
+}
+
 // Work decomposition shared by both attention kernels: a workgroup of 4 waves serves one
 // (sequence, KV head, split); wave w owns tokens [16w, 16w + 16) of every 64-token block of the
 // split (one MFMA tile), so each wave keeps its own online-softmax state over its tiles and the

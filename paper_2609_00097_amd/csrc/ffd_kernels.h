@@ -26,6 +26,7 @@ struct ScanArgs {
     uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, per scan split
     int* counts;                // [B*Hkv, S1]: kept blocks per scan split
     float* shat;                // [B, Hkv, Lcap/64, 4, NT, 64]: scan scores of kept blocks
+    float* sigma;               // top-k selection: block scores [B*Hkv, Lcap/64, G]
     uint8_t* mask;              // [B, Hq, Lcap/64] or null
     float* m_tilde;             // [B, Hq] or null: the pseudo-max of each head
     int Hq, Hkv, Lcap, G, S1;
@@ -35,6 +36,7 @@ struct ScanArgs {
 
 struct RefineArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
+    const uint32_t* codes;      // thumbnail codes: read when the scan scores are recomputed (top-k)
     const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
     const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]
     const uint16_t* v;          // bf16 [B, Hkv, Lcap, 128]
@@ -49,6 +51,17 @@ struct RefineArgs {
     int Hq, Hkv, Lcap, G, S1, W, npairs;
     float scale;
     float top_level;            // Lv of the thumbnail depth: the residual step is M / (254 Lv)
+};
+
+// Fixed-budget (top-k) selection over the block scores the scan kernel wrote; its output takes the
+// place of the scan's kept lists and counts (each group's whole list in split 0).
+struct TopkArgs {
+    const float* sigma;         // [B*Hkv, Lcap/64, G]
+    const int32_t* seq_lens;    // [B]
+    uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, in block order
+    int* counts;                // [B*Hkv, S1]: the list length in split 0, zero elsewhere
+    uint8_t* mask;              // [B, Hq, Lcap/64] or null
+    int Hq, Hkv, Lcap, S1, k;
 };
 
 struct DenseArgs {
@@ -83,10 +96,17 @@ struct AppendArgs {
     int Hkv, Lcap;
 };
 
-// REFINED_PM: the pseudo-max is taken over the window tokens' refined logits (Eq. 3's reading)
-// instead of their thumbnail scores.
-template <int NT, int BITS, bool REFINED_PM> __global__ void ffd_scan_kernel(ScanArgs a);
-template <int NT> __global__ void ffd_refine_kernel(RefineArgs a);
+// What the scan kernel does after scoring a block:
+//  kSelThumbnailPM  top-delta against the pseudo-max of the window tokens' thumbnail scores (Alg. 1);
+//  kSelRefinedPM    top-delta against the pseudo-max of their refined logits (Eq. 3's reading);
+//  kSelTopK         no decision: the block scores go to the workspace for ffd_topk_select_kernel.
+enum ScanMode { kSelThumbnailPM = 0, kSelRefinedPM = 1, kSelTopK = 2 };
+template <int NT, int BITS, int MODE> __global__ void ffd_scan_kernel(ScanArgs a);
+// RBITS = 0: the scan scores of kept blocks come from the workspace; RBITS = b: they are recomputed
+// from the b-bit codes (after a top-k selection, which the scan could not anticipate).
+template <int NT, int RBITS> __global__ void ffd_refine_kernel(RefineArgs a);
+template <int G> __global__ void ffd_topk_select_kernel(TopkArgs a);
+constexpr int kTopkSelectThreads = 1024;
 template <int NT> __global__ void dense_decode_kernel(DenseArgs a);
 template <int BITS> __global__ void quantize_keys_kernel(QuantArgs a);
 template <int BITS> __global__ void append_kv_kernel(AppendArgs a);

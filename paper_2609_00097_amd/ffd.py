@@ -45,8 +45,9 @@ PSEUDO_MAX = {"thumbnail": 0, "refined": 1}     # FFD_PSEUDO_MAX_THUMBNAIL, FFD_
 
 
 class DecodeExtras(ctypes.Structure):
-    """``ffd_decode_extras``: stage events, the pseudo-max output and the pseudo-max source."""
-    _fields_ = [("stage_events", P), ("m_tilde", P), ("pseudo_max", I)]
+    """``ffd_decode_extras``: stage events, the pseudo-max output, the pseudo-max source and the
+    fixed-budget (top-k) selection."""
+    _fields_ = [("stage_events", P), ("m_tilde", P), ("pseudo_max", I), ("top_k", I)]
 
 
 def lib() -> ctypes.CDLL:
@@ -208,7 +209,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
                      n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
                      return_lse: bool = True, return_mask: bool = False, workspace=None,
                      out=None, lse=None, mask=None, stage_events=None, m_tilde=None,
-                     pseudo_max: str = "thumbnail"):
+                     pseudo_max: str = "thumbnail", top_k: int = 0):
     """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested).
     The thumbnail depth is that of ``codes`` (its last dimension is 4 words per bit).
 
@@ -216,7 +217,9 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
     they exist), which the library records before the scan kernel, after it, after the refinement
     kernel and after the merge. ``m_tilde``: optional float32 ``[B, Hq]`` receiving each head's
     pseudo-max. ``pseudo_max``: ``"thumbnail"`` (default) or ``"refined"``, the scores of the window
-    tokens the pseudo-max is taken over."""
+    tokens the pseudo-max is taken over. ``top_k > 0`` replaces the top-delta rule by the fixed
+    budget of ``top_k`` blocks per head (largest thumbnail block scores, ties in block order); delta
+    and the windows are then unused and ``m_tilde`` must be None."""
     B, Hq, D = q.shape
     Hkv, Lcap = v.shape[1], v.shape[2]
     _need(q, "q", torch.bfloat16)
@@ -237,7 +240,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
             raise ValueError("stage_events must be four recorded torch.cuda.Event objects")
         ev = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
     extras = DecodeExtras(ctypes.cast(ev, P) if ev is not None else None, _ptr(m_tilde),
-                          PSEUDO_MAX[pseudo_max])
+                          PSEUDO_MAX[pseudo_max], int(top_k))
     _check("ffd_decode_attention", lib().ffd_decode_attention_ex(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
         D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),

@@ -124,3 +124,16 @@ def test_extras_pseudo_max_source_checked_before_launch(so):
     assert so.ffd_decode_attention_ex(*args, ctypes.byref(bad)) == 1
     mis = ffd.DecodeExtras(None, fake + 2, 0)          # misaligned m_tilde
     assert so.ffd_decode_attention_ex(*args, ctypes.byref(mis)) == 1
+
+
+def test_extras_top_k_checked_before_launch(so):
+    """top_k < 0, or top_k > 0 together with an m_tilde output, is rejected before any launch."""
+    from paper_2609_00097_amd import ffd
+    fake = 0x1000
+    args = [fake] * 6 + [1, 32, 8, 4096, 128, 2, 64, 5.0, 64, 256, 0, 0.0, fake, None, None, fake, 1 << 30, None]
+    neg = ffd.DecodeExtras(None, None, 0, -1)
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(neg)) == 1
+    with_mt = ffd.DecodeExtras(None, fake, 0, 8)
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(with_mt)) == 1
+    # the struct the binding passes has the header's four fields, in order
+    assert [f[0] for f in ffd.DecodeExtras._fields_] == ["stage_events", "m_tilde", "pseudo_max", "top_k"]
