@@ -10,7 +10,10 @@ using namespace ffd;
 
 namespace {
 
-constexpr int kTargetWorkgroups = 512;    // two per CU on 256 CUs
+// Automatic split count: the FFD refinement grid has W + B*Hkv = (S + 1) * B*Hkv workgroups of equal
+// work, which should not exceed two per CU on the 256 CUs: a third workgroup on a few CUs makes those
+// CUs finish last (at 4 x 128K, delta 7: 544 workgroups 148 us, 480 workgroups 133 us).
+constexpr int kTargetWorkgroups = 512;
 constexpr int kMinBlocksPerSplit = 8;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -19,7 +22,7 @@ int resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
     if (num_splits > 0) return num_splits;
     const long long pairs = (long long)B * Hkv;
-    long long s = (kTargetWorkgroups + pairs - 1) / pairs;
+    long long s = kTargetWorkgroups / pairs - 1;
     const long long cap = (long long)(Lcap / FFD_BLOCK) / kMinBlocksPerSplit;
     if (s > cap) s = cap;
     if (s < 1) s = 1;

@@ -43,7 +43,7 @@ def test_status_strings(so):
 
 
 def test_splits_and_workspace_sizes(so):
-    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 16           # about 512 workgroups
+    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 15           # (15 + 1) * 32 = 512 refinement workgroups
     assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
@@ -52,14 +52,14 @@ def test_splits_and_workspace_sizes(so):
     up = lambda x: -(-x // 256) * 256
     P, G, C = 32, 4, 2048
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
-        up((16 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 32 * 4) + up(P * C * 4)
+        up((15 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 32 * 4) + up(P * C * 4)
         + P * C * 1024)
     P, G, C = 2, 8, 64
     assert so.ffd_workspace_bytes(1, 16, 2, 4096, 128, 3) == (
         up((3 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 4 * 4) + up(P * C * 4)
         + P * C * 2048)
     assert so.ffd_workspace_bytes(1, 8, 8, 1 << 25, 128, 1) == 0         # Lcap beyond 2^24 tokens
-    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 16 * 130 * 4
+    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 15 * 130 * 4
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
     assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
 
