@@ -382,7 +382,12 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
     // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
-    // draining every load in flight. Order: queries, pseudo-max window blocks, the first ring round.
+    // draining every load in flight. Order: queries, pseudo-max window blocks, the first ring round;
+    // with kDefer the window blocks come after the first ring round, whose blocks are scored before
+    // the window pass and decided after it. (Every workgroup's first round is in flight when the
+    // window blocks are requested, so they arrive late -- 6 us at the median, 20 us at worst at
+    // 4 x 128K; scoring the first round meanwhile and refilling its slots keeps the stream going.)
+    constexpr bool kDefer = BITS == 2 && NT == 1 && !kTopK;
     uint32_t qw[NT];
     load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
     const int jlast = max(nblk, 1) - 1;
@@ -393,18 +398,30 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
     BlockScan<BITS> win[kPMW];
-    if constexpr (!kTopK) {
+    auto load_windows = [&]() {
 #pragma unroll
         for (int i = 0; i < kPMW; ++i)
             win[i] = load_block_scan<BITS>(codes_bh, absmax_bh,
                                            min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
-    }
+    };
+    if constexpr (!kTopK && !kDefer) load_windows();
     BlockScan<BITS> ring[kRing];
 #pragma unroll
     for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
+    if constexpr (kDefer) load_windows();
 
     HeadConsts<NT> hc;
     build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
+
+    // the first round's scores (kDefer), decided once the pseudo-max is known
+    float first[kDefer ? kRing : 1][NT][4];
+    if constexpr (kDefer) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+            if (r < nbw) block_scores<NT, BITS>(ring[r], jw0 + r, lane, L, hc, first[r]);
+            if (kRing < nbw) ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + r + kRing, jclamp), lane);
+        }
+    }
 
     // ---- pseudo-max over sink and local windows (Eq. 3) ----------------------------------
     // (not needed by the top-k rule, which compares block scores with each other)
@@ -457,9 +474,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
     int nkept = 0;                                  // wave-uniform
-    auto decide = [&](const BlockScan<BITS>& blk, int j) {
-        float sc[NT][4];
-        block_scores<NT, BITS>(blk, j, lane, L, hc, sc);
+    auto decide_scores = [&](const float (&sc)[NT][4], int j) {
         if constexpr (kTopK) {
             float* sigma_bh = a.sigma + bh * (size_t)nblk_cap * G;
             // sigma only: + 0 turns a -0 score (a zero key) into +0, so equal scores compare equal
@@ -491,10 +506,21 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
             ++nkept;
         }
     };
+    auto decide = [&](const BlockScan<BITS>& blk, int j) {
+        float sc[NT][4];
+        block_scores<NT, BITS>(blk, j, lane, L, hc, sc);
+        decide_scores(sc, j);
+    };
     // Every round but the last refills each slot with the block kRing ahead (clamped to the wave's
     // own last block, which is then still cached); the last round issues no loads, so no wave waits
     // on a load it does not use.
     int i0 = 0;
+    if constexpr (kDefer) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r)
+            if (r < nbw) decide_scores(first[r], jw0 + r);
+        i0 = kRing;
+    }
     for (; i0 + kRing < nbw; i0 += kRing) {
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
