@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--context-sweep", default="",
                     help="comma-separated context lengths in K (e.g. 4,8,16,32,64,128,256): "
                          "workload 2's layout at each length, FFD vs dense")
+    ap.add_argument("--workload-sweep", action="store_true",
+                    help="also time FFD and dense on all five workloads at each of their deltas")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-fidelity", action="store_true", help="skip the fidelity diagnostics")
     ap.add_argument("--depths", default="4,8",
@@ -445,6 +447,36 @@ def context_sweep(lengths_k, splits, flush_mib, delta, steps, graph):
     return out
 
 
+def workload_sweep(splits, flush_mib, steps):
+    """FFD and dense step times for workloads 1..5 (each at its deltas), keep ratios, algorithmic TB/s."""
+    import torch
+
+    import ffd_inputs as I
+    out = {}
+    for wl in range(1, 6):
+        case = I.workload(wl)
+        r = Runner(case, splits, flush_mib)
+        d_ms, _ = r.time(r.dense_step, steps, 3)
+        d_us = float(d_ms.mean() * 1e3)
+        entry = {"dense_us": round(d_us, 2),
+                 "dense_tbps": round(dense_bytes(case, r.S) / (d_us * 1e-6) / 1e12, 3)}
+        for delta in case.deltas:
+            keep = r.mask_for(delta)
+            nb = algorithmic_bytes(case, keep, r.S)
+            f_ms, _ = r.time(lambda: r.ffd_step(delta), steps, 5)
+            f_us = float(f_ms.mean() * 1e3)
+            valid = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel() for b in range(case.B)])
+            entry[f"delta={delta:g}"] = {
+                "ffd_us": round(f_us, 2), "speedup_vs_dense": round(d_us / f_us, 2),
+                "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
+                "keep_head_blocks": round(float(valid.mean()), 5),
+                "keep_union_tokens": round(nb["gather_tokens"] / float(case.seq_lens.sum() * case.Hkv), 5)}
+        out[case.name] = entry
+        del r
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -582,6 +614,11 @@ def main():
         torch.cuda.empty_cache()
         line["context_sweep"] = context_sweep([int(x) for x in args.context_sweep.split(",") if x.strip()],
                                               args.splits, args.flush_mib, args.delta, 30, args.graph)
+    if args.workload_sweep:
+        if "r" in locals():
+            del r
+        torch.cuda.empty_cache()
+        line["workload_sweep"] = workload_sweep(args.splits, args.flush_mib, 30)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(case, args.delta, args.cpu_seconds)
     print(json.dumps(line))

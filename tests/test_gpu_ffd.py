@@ -179,3 +179,30 @@ def test_full_size_workloads_sampled(wl, heads):
     for b, L in enumerate(c.seq_lens):
         if L > 0:
             assert keep[b].any(axis=-1).all()
+
+
+def test_maximum_capacity():
+    """The library's largest cache, Lcap = 2^24 tokens: grids and workspace are sized by the capacity
+    (256 scan workgroups per KV group, most with nothing to scan); two sequences in it, one ragged,
+    against the oracle. Tokens past the sequences are zero and never read."""
+    from paper_2609_00097_amd import ffd
+    c = I.small_case(seed=97, B=2, Hq=4, Hkv=1, seq_lens=(3000, 70001), Lcap=70016, heavy_frac=0.03)
+    print("case maximum capacity Lcap=2^24", flush=True)
+    up = Uploaded(c)
+    cap = 1 << 24
+    k = torch.zeros((c.B, c.Hkv, cap, 128), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
+    k[:, :, :c.Lcap] = up.k
+    v[:, :, :c.Lcap] = up.v
+    qk = ffd.quantize_keys(k)
+    out, lse, mask = ffd.decode_attention(up.q, *qk, v, up.seq_lens, delta=5.0, return_lse=True,
+                                          return_mask=True)
+    torch.cuda.synchronize()
+    nb = c.Lcap // 64
+    assert not mask[:, :, nb:].any()
+    near, flipped = compare_ffd(c, 5.0, out, lse, mask[:, :, :nb].contiguous())
+    print(f"near-threshold blocks {near}, flipped {flipped}")
+    dense_out, dense_lse = ffd.dense_decode_attention(up.q, k, v, up.seq_lens)
+    torch.cuda.synchronize()
+    from tests.gpu_util import compare_dense
+    compare_dense(c, dense_out, dense_lse)

@@ -199,3 +199,24 @@ def test_full_size_workloads_sampled(wl, k, heads):
         nb = -(-int(L) // 64)
         assert np.all(keep[b, :, :nb].sum(-1) == min(k, nb))
     print(f"near-threshold blocks {near}, flipped {flipped}")
+
+
+def test_maximum_capacity():
+    """Top-k in the library's largest cache (Lcap = 2^24 tokens); at G = 8 the 70001-token sequence's
+    1094 block scores per head span two of the selection kernel's 1024-block tiles."""
+    from paper_2609_00097_amd import ffd
+    c = I.small_case(seed=101, B=2, Hq=8, Hkv=1, seq_lens=(3000, 70001), Lcap=70016, heavy_frac=0.03)
+    print("case top-k maximum capacity Lcap=2^24", flush=True)
+    up = Uploaded(c)
+    cap = 1 << 24
+    k = torch.zeros((c.B, c.Hkv, cap, 128), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
+    k[:, :, :c.Lcap] = up.k
+    v[:, :, :c.Lcap] = up.v
+    qk = ffd.quantize_keys(k)
+    up2 = Uploaded(c)
+    up2.k, up2.v = k, v
+    out, lse, mask = _run(up2, qk, 29)
+    nb = c.Lcap // 64
+    assert not mask[:, :, nb:].any()
+    compare_topk(c, 29, out, lse, mask[:, :, :nb].contiguous())
