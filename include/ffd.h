@@ -134,9 +134,8 @@ int ffd_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_c
  *   block_mask   uint8 [B, Hq, Lcap/64] or NULL: 1 iff head h kept block j; 0 at/after the end.
  *   workspace    device scratch of at least ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)
  *                bytes: the partials, a per-KV-group table locating them, the scan's kept-block
- *                lists and counts, and the scan scores of kept blocks (written by the scan kernel,
- *                read by the refinement kernel; 1 KiB per block for G <= 4, 2 KiB for G = 8,
- *                reserved for every block of the capacity). It needs no initialisation and is
+ *                lists and counts, and the per-head block scores the top-k rule selects from
+ *                (4 * G bytes per block of the capacity). It needs no initialisation and is
  *                clobbered. Calls that overlap in time (different streams) need separate workspaces.
  *  Limits: B * Hkv <= 2^20 and Lcap <= 2^24 tokens, else FFD_ERR_UNSUPPORTED.
  */
@@ -209,7 +208,7 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
  * point too). With S = ffd_resolve_splits(...), P = B * Hkv KV groups, G = Hq / Hkv, C = Lcap / 64
  * blocks and S1 scan splits per group (chosen by the library from B, Hkv, Lcap), the regions, each
  * starting on a 256-byte boundary, are: partials (S * P + P) * G * (D + 2) * 4 bytes, table P * 8,
- * kept counts P * S1 * 4, kept lists P * C * 4, scan scores P * C * 1024 * (G <= 4 ? 1 : 2).
+ * kept counts P * S1 * 4, kept lists P * C * 4, block scores P * C * G * 4.
  * 0 on invalid or unsupported input. */
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
 

@@ -54,7 +54,7 @@ int launch_status() {
 }
 
 // Workspace: split partials m [B,Hq,S], l [B,Hq,S], acc [B,Hq,S,D] (fp32); the FFD path adds the
-// scan kernel's per-block keep bits and the scan scores of kept blocks.
+// scan kernel's kept lists and counts and the top-k rule's block scores.
 struct Partials {
     float* m;
     float* l;
@@ -97,10 +97,10 @@ int scan_splits(int B, int Hkv, int Lcap) {
 
 // FFD workspace: partials for W + B*Hkv refinement workgroups (W = S * B * Hkv) of G heads each,
 // the per-group (first workgroup, count) table, the scan's per-split kept counts and kept lists,
-// and the scan scores of kept blocks.
+// and the block scores [P, C, G] that the top-k rule selects from.
 struct FfdWorkspace {
     size_t rows;                      // partial rows
-    size_t table_off, counts_off, lists_off, shat_off, total;
+    size_t table_off, counts_off, lists_off, sigma_off, total;
 };
 
 FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
@@ -111,8 +111,8 @@ FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
     w.table_off = round_up(w.rows * (D + 2) * sizeof(float), kAlign);
     w.counts_off = w.table_off + round_up(pairs * 2 * sizeof(int), kAlign);
     w.lists_off = w.counts_off + round_up(pairs * scan_splits(B, Hkv, Lcap) * sizeof(int), kAlign);
-    w.shat_off = w.lists_off + round_up(pairs * nblk_cap * sizeof(uint32_t), kAlign);
-    w.total = w.shat_off + pairs * nblk_cap * 4 * head_tiles(Hq / Hkv) * 64 * sizeof(float);
+    w.sigma_off = w.lists_off + round_up(pairs * nblk_cap * sizeof(uint32_t), kAlign);
+    w.total = w.sigma_off + pairs * nblk_cap * (size_t)(Hq / Hkv) * sizeof(float);
     return w;
 }
 
@@ -158,11 +158,10 @@ void launch_scan(int bits, int nt, int mode, dim3 grid, hipStream_t stream, cons
     else launch_scan_bits<8>(nt, mode, grid, stream, sa);
 }
 
-// The refinement kernel: scan scores from the workspace (rbits = 0) or recomputed from rbits-bit codes.
+// The refinement kernel, recomputing the scan scores from rbits-bit codes.
 template <int NT>
 void launch_refine_nt(int rbits, dim3 grid, hipStream_t stream, const RefineArgs& ra) {
-    if (rbits == 0) hipLaunchKernelGGL((ffd_refine_kernel<NT, 0>), grid, dim3(kThreads), 0, stream, ra);
-    else if (rbits == 2) hipLaunchKernelGGL((ffd_refine_kernel<NT, 2>), grid, dim3(kThreads), 0, stream, ra);
+    if (rbits == 2) hipLaunchKernelGGL((ffd_refine_kernel<NT, 2>), grid, dim3(kThreads), 0, stream, ra);
     else if (rbits == 4) hipLaunchKernelGGL((ffd_refine_kernel<NT, 4>), grid, dim3(kThreads), 0, stream, ra);
     else hipLaunchKernelGGL((ffd_refine_kernel<NT, 8>), grid, dim3(kThreads), 0, stream, ra);
 }
@@ -285,20 +284,17 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     int2* table = reinterpret_cast<int2*>(ws + W.table_off);
     int* counts = reinterpret_cast<int*>(ws + W.counts_off);
     uint32_t* lists = reinterpret_cast<uint32_t*>(ws + W.lists_off);
-    float* shat = reinterpret_cast<float*>(ws + W.shat_off);
+    float* sigma = reinterpret_cast<float*>(ws + W.sigma_off);
     const int S1 = scan_splits(B, Hkv, Lcap);
     const int npairs = B * Hkv;
     const int Wr = S * npairs;
-    // top-k: the block scores [P, C, G] take the place of the kept blocks' scan scores (which the
-    // refinement then recomputes from the codes)
-    float* sigma = shat;
     ScanArgs sa{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
                 static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid), seq_lens, lists,
-                counts, shat, sigma, block_mask, m_tilde, Hq, Hkv, Lcap, G, S1, delta, scale, n_sink, n_local};
+                counts, sigma, block_mask, m_tilde, Hq, Hkv, Lcap, G, S1, delta, scale, n_sink, n_local};
     RefineArgs ra{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
                   static_cast<const uint16_t*>(k_absmax),
                   static_cast<const int8_t*>(k_resid), static_cast<const uint16_t*>(v), seq_lens, lists,
-                  counts, shat, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale,
+                  counts, table, part_m, part_l, part_acc, Hq, Hkv, Lcap, G, S1, Wr, npairs, scale,
                   thumb_top_level(thumb_bits)};
     TopkArgs ta{sigma, seq_lens, lists, counts, block_mask, Hq, Hkv, Lcap, S1, top_k};
     const dim3 scan_grid((unsigned)S1, (unsigned)Hkv, (unsigned)B);
@@ -321,9 +317,8 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
         if ((st = launch_status()) != FFD_OK) return st;
     }
     if ((st = mark(1)) != FFD_OK) return st;
-    const int rbits = top_k > 0 ? thumb_bits : 0;
-    if (G <= 4) launch_refine_nt<1>(rbits, refine_grid, stream, ra);
-    else launch_refine_nt<2>(rbits, refine_grid, stream, ra);
+    if (G <= 4) launch_refine_nt<1>(thumb_bits, refine_grid, stream, ra);
+    else launch_refine_nt<2>(thumb_bits, refine_grid, stream, ra);
     if ((st = launch_status()) != FFD_OK || (st = mark(2)) != FFD_OK) return st;
     hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, part_m, part_l,
                        part_acc, 0, table, G, static_cast<uint16_t*>(out), lse);

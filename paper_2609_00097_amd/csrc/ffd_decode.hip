@@ -21,14 +21,18 @@
 //
 // Two kernels, so that each stage's HBM stream is balanced over the whole chip:
 //  * ffd_scan_kernel streams the codes and absmaxes of every block once (the dominant, perfectly
-//    regular stream) and takes the keep decision per (head, block). For each kept block it stores
-//    the scan scores s_hat (the Eq. 4 reuse term) and appends the block, with its per-head keep bits,
-//    to its workgroup's kept list (in block order) in the workspace, plus the list's length.
+//    regular stream), keeps each block's per-head maximum score in LDS and, once its stream and the
+//    pseudo-max are done, takes the keep decision per (head, block): the kept blocks, with their
+//    per-head keep bits, form its workgroup's kept list (in block order) in the workspace, plus the
+//    list's length.
 //  * ffd_refine_kernel gives each (sequence, KV head) a number of workgroups proportional to its
 //    kept blocks (every workgroup computes the same allocation from the scan's counts, so no
 //    cross-workgroup synchronisation is needed); each workgroup refines an equal share of its KV
 //    group's kept blocks, wave w taking 16-token tile w of every block, with several tiles' residual
-//    and value loads in flight, and writes one partial (m, l, acc) per head. lse_merge_kernel
+//    and value loads in flight, recomputes the scan scores s_hat of each tile from its codes (Eq. 4's
+//    reuse term: the same integer MFMA and fp32 operations as the scan, so the same values; storing
+//    them would cost as many bytes, written then read), and writes one partial (m, l, acc) per
+//    head. lse_merge_kernel
 //    combines the partials of each head, located through a small per-group table.
 #include "ffd_device.h"
 #include "ffd_kernels.h"
@@ -50,7 +54,6 @@ constexpr int kRing2 = FFD_SCAN_RING;         // 2-bit scan loads in flight per 
 constexpr int kPMW2 = 2;                      // 2-bit pseudo-max window blocks per wave per pass
 constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
 constexpr int kChunk = kFfdChunk;             // list entries staged per pass of the refinement kernel
-constexpr int kWaveList = kFfdMaxScanBlocks / kWaves;   // kept blocks one scan wave can hold
 
 __device__ __forceinline__ int limb_of(int Q, int which) {
     const int l0 = ((Q + 128) & 255) - 128;
@@ -228,29 +231,27 @@ __device__ __forceinline__ void block_scores(const BlockScan<BITS>& ld, int j, i
 template <int NT>
 struct ScanLds {
     QueryLds<NT> qs;
-    float pm[kWaves][4 * NT];
-    uint32_t kept[kWaves][kWaveList];    // each wave's kept blocks, in block order
-    int nkept[kWaves];
+    alignas(16) float pm[kWaves][4 * NT];                 // each wave's window maxima per head
+    alignas(16) float sig[kFfdMaxScanBlocks][4 * NT];     // block maxima of the thumbnail scores per head
+    int nkept[kWaves];                        // kept blocks per wave
 };
 
 // ---- refinement helpers ---------------------------------------------------------------------
 
 // One wave's loads for one 16-token tile of a kept block: int8 residual, its lane's value dwords,
-// the token's absmax, and either the stored scan scores of its heads (RBITS = 0) or the lane's
-// RBITS code words of the tile, from which the scan scores are recomputed.
+// the token's absmax and the lane's RBITS code words of the tile, from which the scan scores are
+// recomputed.
 template <int NT, int RBITS>
 struct RefineTile {
     v4i r0, r1;
     VTile vt;
-    float sc[RBITS == 0 ? NT : 1];
-    uint32_t cw[RBITS == 0 ? 1 : RBITS];
+    uint32_t cw[RBITS];
     uint32_t m;       // absmax bf16 bits in the low half
 };
 
 template <int NT, int RBITS>
 __device__ __forceinline__ RefineTile<NT, RBITS> load_refine_tile(const int8_t* __restrict__ resid_bh,
                                                                   const uint16_t* __restrict__ v_bh,
-                                                                  const float* __restrict__ shat_bh,
                                                                   const uint32_t* __restrict__ codes_bh,
                                                                   const uint16_t* __restrict__ absmax_bh,
                                                                   int j, int T4, int lane, int last_row) {
@@ -260,22 +261,16 @@ __device__ __forceinline__ RefineTile<NT, RBITS> load_refine_tile(const int8_t* 
     r.r0 = rp[0];
     r.r1 = rp[64];
     r.vt = load_vtile(v_bh, 16 * tile, last_row, lane);
-    if constexpr (RBITS == 0) {
-        const float* sp = shat_bh + (size_t)tile * (NT * 64) + lane;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) r.sc[t] = sp[64 * t];
+    // the lane's 4b words of block j; tile T4 is words T4*b .. T4*b + b - 1
+    const uint32_t* cp = codes_bh + ((size_t)j * 64 + lane) * (4 * RBITS) + T4 * RBITS;
+    if constexpr (RBITS == 2) {
+        const uint2 w = *reinterpret_cast<const uint2*>(cp);
+        r.cw[0] = w.x; r.cw[1] = w.y;
     } else {
-        // the lane's 4b words of block j; tile T4 is words T4*b .. T4*b + b - 1
-        const uint32_t* cp = codes_bh + ((size_t)j * 64 + lane) * (4 * RBITS) + T4 * RBITS;
-        if constexpr (RBITS == 2) {
-            const uint2 w = *reinterpret_cast<const uint2*>(cp);
-            r.cw[0] = w.x; r.cw[1] = w.y;
-        } else {
 #pragma unroll
-            for (int i = 0; i < RBITS / 4; ++i) {
-                const uint4 w = reinterpret_cast<const uint4*>(cp)[i];
-                r.cw[4 * i] = w.x; r.cw[4 * i + 1] = w.y; r.cw[4 * i + 2] = w.z; r.cw[4 * i + 3] = w.w;
-            }
+        for (int i = 0; i < RBITS / 4; ++i) {
+            const uint4 w = reinterpret_cast<const uint4*>(cp)[i];
+            r.cw[4 * i] = w.x; r.cw[4 * i + 1] = w.y; r.cw[4 * i + 2] = w.z; r.cw[4 * i + 3] = w.w;
         }
     }
     r.m = absmax_bh[(size_t)j * 64 + (lane & 15) * 4 + T4];
@@ -303,8 +298,8 @@ struct RefineLds {
 }  // namespace
 
 // ================================================================================================
-// Scan: pseudo-max, b-bit thumbnail scan, keep decision; scan scores and the kept list to the
-// workspace.
+// Scan: b-bit thumbnail scan and pseudo-max, then the keep decisions; the kept list (or, for the
+// top-k rule, every block's scores) to the workspace.
 // Grid (S1, Hkv, B); workgroup s1 scans blocks [s1 * bps, (s1 + 1) * bps) of one (sequence, KV
 // head), bps = ceil(nblk / S1) <= kFfdMaxScanBlocks; wave w takes a contiguous quarter of them and
 // keeps kRing blocks in flight.
@@ -341,9 +336,10 @@ __device__ __forceinline__ void add_residual_term(const int8_t* __restrict__ res
     }
 }
 
-// Workgroups per CU: the 8-bit blocks and the refined pseudo-max's residual tiles need more registers.
+// Workgroups per CU (a lower bound that caps registers at 512 / (4 n) per lane): the 8-bit blocks,
+// and for eight heads the 4-bit blocks or the refined pseudo-max's residual tiles, need more registers.
 template <int NT, int BITS, int MODE> constexpr int scan_occupancy() {
-    return BITS == 8 ? 2 : (MODE == kSelRefinedPM ? (NT == 1 ? 3 : 2) : 4);
+    return BITS == 8 ? 2 : (NT == 2 && (BITS == 4 || MODE == kSelRefinedPM) ? 3 : 4);
 }
 
 template <int NT, int BITS, int MODE>
@@ -372,7 +368,6 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * BITS);
     const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
-    float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
 
     // This wave's blocks: [jw0, jw0 + nbw).
     const int qw_blocks = (bps + kWaves - 1) / kWaves;
@@ -382,12 +377,13 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
     // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
-    // draining every load in flight. Order: queries, pseudo-max window blocks, the first ring round;
-    // with kDefer the window blocks come after the first ring round, whose blocks are scored before
-    // the window pass and decided after it. (Every workgroup's first round is in flight when the
-    // window blocks are requested, so they arrive late -- 6 us at the median, 20 us at worst at
-    // 4 x 128K; scoring the first round meanwhile and refilling its slots keeps the stream going.)
-    constexpr bool kDefer = BITS == 2 && NT == 1 && !kTopK;
+    // draining every load in flight. Order: queries, the first ring round, then the window blocks of
+    // the first pseudo-max pass, scored by each wave on its own once its first round is consumed
+    // (with the refined logits, at the end of the stream, after their residual tiles). Every keep
+    // decision waits for the end of the stream, where the pseudo-max is known, so no wave waits on
+    // another in the middle of its stream (every workgroup's first round is in flight when the
+    // window blocks are requested, so a workgroup-wide window pass before the stream waited 6 us at
+    // the median, 20 us at worst at 4 x 128K). Until then a block costs G floats of LDS.
     uint32_t qw[NT];
     load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
     const int jlast = max(nblk, 1) - 1;
@@ -397,146 +393,138 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     const int loc_blk_beg = max(loc_beg / kBlock, sink_blk_end);
     const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
-    BlockScan<BITS> win[kPMW];
-    auto load_windows = [&]() {
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i)
-            win[i] = load_block_scan<BITS>(codes_bh, absmax_bh,
-                                           min(pm_block(min(kWaves * i + wave, max(npm, 1) - 1)), jlast), lane);
-    };
-    if constexpr (!kTopK && !kDefer) load_windows();
+    auto win_block = [&](int idx) { return min(pm_block(min(idx, max(npm, 1) - 1)), jlast); };
     BlockScan<BITS> ring[kRing];
 #pragma unroll
     for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
-    if constexpr (kDefer) load_windows();
+    BlockScan<BITS> win[kPMW];
+    if constexpr (!kTopK) {
+#pragma unroll
+        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(kWaves * i + wave), lane);
+    }
 
     HeadConsts<NT> hc;
     build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
 
-    // the first round's scores (kDefer), decided once the pseudo-max is known
-    float first[kDefer ? kRing : 1][NT][4];
-    if constexpr (kDefer) {
+    // ---- scan (Alg. 1): block maxima sigma per head, and the pseudo-max's window maxima -------
+    float pm[NT];
 #pragma unroll
-        for (int r = 0; r < kRing; ++r) {
-            if (r < nbw) block_scores<NT, BITS>(ring[r], jw0 + r, lane, L, hc, first[r]);
-            if (kRing < nbw) ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + r + kRing, jclamp), lane);
-        }
-    }
-
-    // ---- pseudo-max over sink and local windows (Eq. 3) ----------------------------------
-    // (not needed by the top-k rule, which compares block scores with each other)
-    float thr[NT];
+    for (int t = 0; t < NT; ++t) pm[t] = -INFINITY;
+    auto window_max = [&](const float (&sc)[NT][4], int j) {     // over the window tokens of block j
 #pragma unroll
-    for (int t = 0; t < NT; ++t) thr[t] = -INFINITY;
-    if constexpr (!kTopK) {
-        float pm[NT];
+        for (int T4 = 0; T4 < 4; ++T4) {
+            const int tok = 64 * j + 16 * T4 + n;
+            const bool in_win = tok < L && (tok < sink_end || tok >= loc_beg);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) pm[t] = -INFINITY;
-        for (int base = 0; base < npm; base += kWaves * kPMW) {
-            if (base > 0) {
-#pragma unroll
-                for (int i = 0; i < kPMW; ++i)
-                    win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, pm_block(min(base + kWaves * i + wave, npm - 1)), lane);
-            }
-#pragma unroll
-            for (int i = 0; i < kPMW; ++i) {
-                const int idx = base + kWaves * i + wave;
-                const int j = pm_block(min(idx, npm - 1));
-                float sc[NT][4];
-                block_scores<NT, BITS>(win[i], j, lane, L, hc, sc);
-                if constexpr (MODE == kSelRefinedPM)
-                    add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win[i].mm, j, lane, hc, sc);
-#pragma unroll
-                for (int T4 = 0; T4 < 4; ++T4) {
-                    const int tok = 64 * j + 16 * T4 + n;
-                    const bool in_win = idx < npm && tok < L && (tok < sink_end || tok >= loc_beg);
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
-                }
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            pm[t] = row16_max(pm[t]);
-            if (n == 0) sm.pm[wave][4 * t + g] = pm[t];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            float m = -INFINITY;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][4 * t + g]);
-            thr[t] = m - a.delta;                      // -inf when both windows are empty
-            if (a.m_tilde && s == 0 && wave == 0 && n == 0 && hc.live[t])
-                a.m_tilde[(size_t)b * a.Hq + hq0 + 4 * t + g] = m;
-        }
-    }
-
-    // ---- scan and decide (Alg. 1; Eq. 1) ------------------------------------------------
-    int nkept = 0;                                  // wave-uniform
-    auto decide_scores = [&](const float (&sc)[NT][4], int j) {
-        if constexpr (kTopK) {
-            float* sigma_bh = a.sigma + bh * (size_t)nblk_cap * G;
-            // sigma only: + 0 turns a -0 score (a zero key) into +0, so equal scores compare equal
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3]))) + 0.f;
-                if (n == 0 && hc.live[t]) sigma_bh[(size_t)j * G + 4 * t + g] = sig;
-            }
-            return;
-        }
-        uint32_t bits = 0;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3])));
-            const bool keep = hc.live[t] && sig >= thr[t];
-            if (a.mask && n == 0 && hc.live[t])
-                a.mask[((size_t)b * a.Hq + hq0 + 4 * t + g) * nblk_cap + j] = keep ? 1 : 0;
-            const uint64_t bl = __ballot(keep && n == 0);
-            bits |= (uint32_t)(((bl >> 0) & 1u) | ((bl >> 15) & 2u) | ((bl >> 30) & 4u) |
-                               ((bl >> 45) & 8u)) << (4 * t);
-        }
-        if (bits != 0) {                              // wave-uniform: the block is gathered
-            float* sp = shat_bh + (size_t)j * (4 * NT * 64) + lane;
-#pragma unroll
-            for (int T4 = 0; T4 < 4; ++T4)
-#pragma unroll
-                for (int t = 0; t < NT; ++t) sp[(T4 * NT + t) * 64] = sc[t][T4];
-            if (lane == 0) sm.kept[wave][nkept] = (uint32_t)j | (bits << 24);
-            ++nkept;
+            for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
         }
     };
-    auto decide = [&](const BlockScan<BITS>& blk, int j) {
+    auto window_pass = [&](const BlockScan<BITS> (&wb)[kPMW], int base) {
+#pragma unroll
+        for (int i = 0; i < kPMW; ++i) {
+            const int idx = base + kWaves * i + wave;
+            if (idx >= npm) continue;                   // wave-uniform
+            const int j = pm_block(idx);
+            float sc[NT][4];
+            block_scores<NT, BITS>(wb[i], j, lane, L, hc, sc);
+            if constexpr (MODE == kSelRefinedPM)
+                add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, wb[i].mm, j, lane, hc, sc);
+            window_max(sc, j);
+        }
+    };
+    auto consume = [&](const BlockScan<BITS>& blk, int j) {
         float sc[NT][4];
         block_scores<NT, BITS>(blk, j, lane, L, hc, sc);
-        decide_scores(sc, j);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            // + 0 turns a -0 score (a zero key) into +0, so that equal scores compare equal
+            const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3]))) + 0.f;
+            if constexpr (kTopK) {
+                if (n == 0 && hc.live[t]) a.sigma[(bh * (size_t)nblk_cap + j) * G + 4 * t + g] = sig;
+            } else {
+                if (n == 0) sm.sig[j - jb][4 * t + g] = sig;
+            }
+        }
     };
     // Every round but the last refills each slot with the block kRing ahead (clamped to the wave's
     // own last block, which is then still cached); the last round issues no loads, so no wave waits
     // on a load it does not use.
-    int i0 = 0;
-    if constexpr (kDefer) {
-#pragma unroll
-        for (int r = 0; r < kRing; ++r)
-            if (r < nbw) decide_scores(first[r], jw0 + r);
-        i0 = kRing;
-    }
-    for (; i0 + kRing < nbw; i0 += kRing) {
+    constexpr bool kEarlyWindows = MODE == kSelThumbnailPM;
+    auto ring_round = [&](int i) {
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
-            const int j = jw0 + i0 + r;
-            decide(ring[r], j);
+            const int j = jw0 + i + r;
+            consume(ring[r], j);
             ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
         }
+    };
+    int i0 = 0;
+    if (kEarlyWindows && kRing < nbw) {         // the first round, then the window blocks behind it
+        ring_round(0);
+        window_pass(win, 0);
+        i0 = kRing;
     }
+    for (; i0 + kRing < nbw; i0 += kRing) ring_round(i0);
 #pragma unroll
     for (int r = 0; r < kRing; ++r)
-        if (i0 + r < nbw) decide(ring[r], jw0 + i0 + r);
+        if (i0 + r < nbw) consume(ring[r], jw0 + i0 + r);
 
-    if constexpr (kTopK) return;
+    if constexpr (kTopK) return;                // the top-k rule compares block scores with each other
 
-    // ---- this workgroup's kept list, in block order, and its length ------------------------
-    if (lane == 0) sm.nkept[wave] = nkept;
+    // ---- pseudo-max over the sink and local windows (Eq. 3): the first pass unless done during
+    // the stream, further passes (wide windows) loaded now -------------------------------------
+    if (!kEarlyWindows || kRing >= nbw) window_pass(win, 0);
+    for (int base = kWaves * kPMW; base < npm; base += kWaves * kPMW) {
+#pragma unroll
+        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + kWaves * i + wave), lane);
+        window_pass(win, base);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        pm[t] = row16_max(pm[t]);
+        if (n == 0) sm.pm[wave][4 * t + g] = pm[t];
+    }
+    __syncthreads();
+
+    // ---- decide (Eq. 1) per (head, block): keep iff sigma >= m~ - delta; the workgroup's kept
+    // list in block order, its length and the optional mask -----------------------------------
+    float thr[4 * NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        float4 m = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float4 p = reinterpret_cast<const float4*>(sm.pm[w])[t];
+            m.x = fmaxf(m.x, p.x); m.y = fmaxf(m.y, p.y); m.z = fmaxf(m.z, p.z); m.w = fmaxf(m.w, p.w);
+        }
+        thr[4 * t] = m.x - a.delta;                     // -inf when both windows are empty
+        thr[4 * t + 1] = m.y - a.delta;
+        thr[4 * t + 2] = m.z - a.delta;
+        thr[4 * t + 3] = m.w - a.delta;
+    }
+    if (a.m_tilde && s == 0 && tid < G) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][tid]);
+        a.m_tilde[(size_t)b * a.Hq + hq0 + tid] = m;
+    }
+    // lane i of wave w decides the wave's block jw0 + i (a wave holds at most 64 blocks)
+    uint32_t bits = 0;
+    const int jl = jw0 + lane;
+    if (lane < nbw) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float4 sg = reinterpret_cast<const float4*>(sm.sig[jl - jb])[t];
+            bits |= ((uint32_t)(sg.x >= thr[4 * t]) | (uint32_t)(sg.y >= thr[4 * t + 1]) << 1 |
+                     (uint32_t)(sg.z >= thr[4 * t + 2]) << 2 | (uint32_t)(sg.w >= thr[4 * t + 3]) << 3) << (4 * t);
+        }
+        bits &= (1u << G) - 1u;                         // heads past G are never kept
+        if (a.mask)
+            for (int h = 0; h < G; ++h) a.mask[((size_t)b * a.Hq + hq0 + h) * nblk_cap + jl] = (bits >> h) & 1u;
+    }
+    const uint64_t kept = __ballot(bits != 0);
+    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(kept >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)kept, 0u));
+    if (lane == 0) sm.nkept[wave] = __popcll(kept);
     __syncthreads();
     int before = 0, total = 0;
 #pragma unroll
@@ -545,8 +533,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
         before += w < wave ? c : 0;
         total += c;
     }
-    uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap + jb;
-    for (int k = lane; k < nkept; k += 64) list_bh[before + k] = sm.kept[wave][k];
+    if (bits != 0) a.lists[bh * (size_t)nblk_cap + jb + before + below] = (uint32_t)jl | (bits << 24);
     if (tid == 0) a.counts[bh * a.S1 + s] = total;
 
     // Mask entries past the end of the sequence are zero (spread over the scan workgroups).
@@ -686,8 +673,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
     const int8_t* resid_bh = a.resid + bh * (size_t)a.Lcap * kD;
     const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
-    const float* shat_bh = a.shat + bh * (size_t)nblk_cap * (4 * NT * 64);
-    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * (RBITS == 0 ? 2 : RBITS));
+    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * RBITS);
     const uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap;
 
     uint32_t qw[NT];
@@ -723,13 +709,8 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         float z[NT];
         bool keep[NT];
         const float Mt = bf16_to_f32((uint16_t)rt.m);
-        float shat[NT];
-        if constexpr (RBITS == 0) {
-#pragma unroll
-            for (int t = 0; t < NT; ++t) shat[t] = rt.sc[t];
-        } else {
-            tile_scores<NT, RBITS>(rt.cw, Mt, 64 * j + 16 * wave + n < L, hc, shat);
-        }
+        float shat[NT];                             // Eq. 4's first term: the scan scores, recomputed
+        tile_scores<NT, RBITS>(rt.cw, Mt, 64 * j + 16 * wave + n < L, hc, shat);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             v4i acc = {0, 0, 0, 0};
@@ -767,7 +748,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         RefineTile<NT, RBITS> ring[kRefineRing];
 #pragma unroll
         for (int r = 0; r < kRefineRing; ++r)
-            ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, shat_bh, codes_bh, absmax_bh, block_of(r), wave,
+            ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh, block_of(r), wave,
                                                   lane, last_row);
         // the refill of the last round re-reads the share's last tile (clamped): it is still
         // cached, and a conditional refill would cost more registers than it saves
@@ -776,7 +757,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
             for (int r = 0; r < kRefineRing; ++r) {
                 const int i = i0 + r;
                 if (i < m) attend(ring[r], (int)(sm.u.list[i] & 0xffffffu), sm.u.list[i] >> 24);
-                ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, shat_bh, codes_bh, absmax_bh,
+                ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh,
                                                       block_of(i + kRefineRing), wave, lane, last_row);
             }
         }
@@ -805,8 +786,6 @@ template __global__ void ffd_scan_kernel<1, 4, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<2, 4, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<1, 8, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<2, 8, kSelTopK>(ScanArgs);
-template __global__ void ffd_refine_kernel<1, 0>(RefineArgs);
-template __global__ void ffd_refine_kernel<2, 0>(RefineArgs);
 template __global__ void ffd_refine_kernel<1, 2>(RefineArgs);
 template __global__ void ffd_refine_kernel<2, 2>(RefineArgs);
 template __global__ void ffd_refine_kernel<1, 4>(RefineArgs);

@@ -25,7 +25,6 @@ struct ScanArgs {
     const int32_t* seq_lens;    // [B]
     uint32_t* lists;            // [B*Hkv, Lcap/64]: kept blocks j | keep bits << 24, per scan split
     int* counts;                // [B*Hkv, S1]: kept blocks per scan split
-    float* shat;                // [B, Hkv, Lcap/64, 4, NT, 64]: scan scores of kept blocks
     float* sigma;               // top-k selection: block scores [B*Hkv, Lcap/64, G]
     uint8_t* mask;              // [B, Hq, Lcap/64] or null
     float* m_tilde;             // [B, Hq] or null: the pseudo-max of each head
@@ -36,14 +35,13 @@ struct ScanArgs {
 
 struct RefineArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
-    const uint32_t* codes;      // thumbnail codes: read when the scan scores are recomputed (top-k)
+    const uint32_t* codes;      // thumbnail codes, from which the scan scores are recomputed
     const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
     const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]
     const uint16_t* v;          // bf16 [B, Hkv, Lcap, 128]
     const int32_t* seq_lens;    // [B]
     const uint32_t* lists;      // written by ffd_scan_kernel
     const int* counts;          // written by ffd_scan_kernel
-    const float* shat;          // written by ffd_scan_kernel
     int2* table;                // [B*Hkv]: (first workgroup, workgroups) of each KV group
     float* part_m;              // [(W + B*Hkv) * G]
     float* part_l;
@@ -100,10 +98,11 @@ struct AppendArgs {
 //  kSelThumbnailPM  top-delta against the pseudo-max of the window tokens' thumbnail scores (Alg. 1);
 //  kSelRefinedPM    top-delta against the pseudo-max of their refined logits (Eq. 3's reading);
 //  kSelTopK         no decision: the block scores go to the workspace for ffd_topk_select_kernel.
+// The first two write the kept lists and counts; no mode stores the scan scores.
 enum ScanMode { kSelThumbnailPM = 0, kSelRefinedPM = 1, kSelTopK = 2 };
 template <int NT, int BITS, int MODE> __global__ void ffd_scan_kernel(ScanArgs a);
-// RBITS = 0: the scan scores of kept blocks come from the workspace; RBITS = b: they are recomputed
-// from the b-bit codes (after a top-k selection, which the scan could not anticipate).
+// The scan scores of the kept tiles (Eq. 4's first term) are recomputed from the RBITS-bit codes with
+// the scan kernel's own integer MFMA and fp32 operations, so they equal the scan's bit for bit.
 template <int NT, int RBITS> __global__ void ffd_refine_kernel(RefineArgs a);
 template <int G> __global__ void ffd_topk_select_kernel(TopkArgs a);
 constexpr int kTopkSelectThreads = 1024;
