@@ -377,13 +377,14 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
     // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
-    // draining every load in flight. Order: queries, the first ring round, then the window blocks of
-    // the first pseudo-max pass, scored by each wave on its own once its first round is consumed
-    // (with the refined logits, at the end of the stream, after their residual tiles). Every keep
-    // decision waits for the end of the stream, where the pseudo-max is known, so no wave waits on
-    // another in the middle of its stream (every workgroup's first round is in flight when the
-    // window blocks are requested, so a workgroup-wide window pass before the stream waited 6 us at
-    // the median, 20 us at worst at 4 x 128K). Until then a block costs G floats of LDS.
+    // draining every load in flight. Order: queries, the window blocks of the first pseudo-max pass,
+    // the first ring round. Each wave scores its window blocks on its own before its first block
+    // (the refined logits: after the stream, with the window blocks' residual tiles) and only
+    // writes their maxima to LDS; every keep decision waits for the end of the stream, where the
+    // pseudo-max is known, so no wave waits on another before or during its stream (a
+    // workgroup-wide window pass before the stream held every wave until the slowest one's window
+    // blocks had arrived behind the whole chip's first round: 6 us at the median, 20 us at worst at
+    // 4 x 128K). Until then a block costs G floats of LDS.
     uint32_t qw[NT];
     load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
     const int jlast = max(nblk, 1) - 1;
@@ -394,14 +395,17 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
     auto win_block = [&](int idx) { return min(pm_block(min(idx, max(npm, 1) - 1)), jlast); };
+    constexpr bool kEarlyWindows = MODE == kSelThumbnailPM;
+    BlockScan<BITS> win[kPMW];
+    auto load_windows = [&](int base) {
+#pragma unroll
+        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + kWaves * i + wave), lane);
+    };
+    if constexpr (kEarlyWindows) load_windows(0);
     BlockScan<BITS> ring[kRing];
 #pragma unroll
     for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
-    BlockScan<BITS> win[kPMW];
-    if constexpr (!kTopK) {
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(kWaves * i + wave), lane);
-    }
+    if constexpr (MODE == kSelRefinedPM) load_windows(0);
 
     HeadConsts<NT> hc;
     build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
@@ -449,7 +453,6 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     // Every round but the last refills each slot with the block kRing ahead (clamped to the wave's
     // own last block, which is then still cached); the last round issues no loads, so no wave waits
     // on a load it does not use.
-    constexpr bool kEarlyWindows = MODE == kSelThumbnailPM;
     auto ring_round = [&](int i) {
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
@@ -458,12 +461,8 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
             ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
         }
     };
+    if constexpr (kEarlyWindows) window_pass(win, 0);   // its blocks arrive ahead of the first round
     int i0 = 0;
-    if (kEarlyWindows && kRing < nbw) {         // the first round, then the window blocks behind it
-        ring_round(0);
-        window_pass(win, 0);
-        i0 = kRing;
-    }
     for (; i0 + kRing < nbw; i0 += kRing) ring_round(i0);
 #pragma unroll
     for (int r = 0; r < kRing; ++r)
@@ -473,10 +472,9 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // ---- pseudo-max over the sink and local windows (Eq. 3): the first pass unless done during
     // the stream, further passes (wide windows) loaded now -------------------------------------
-    if (!kEarlyWindows || kRing >= nbw) window_pass(win, 0);
+    if constexpr (!kEarlyWindows) window_pass(win, 0);
     for (int base = kWaves * kPMW; base < npm; base += kWaves * kPMW) {
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + kWaves * i + wave), lane);
+        load_windows(base);
         window_pass(win, base);
     }
 #pragma unroll
