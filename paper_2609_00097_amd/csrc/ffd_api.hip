@@ -74,13 +74,12 @@ Partials carve(void* ws, int B, int Hq, int S) {
 
 int head_tiles(int G) { return G <= 4 ? 1 : 2; }
 
-// Workgroups of the scan kernel per (sequence, KV head): about kScanWorkgroups in all, each scanning
-// at least kMinScanBlocks blocks so the pseudo-max and query setup stay a small part of its work, and
-// at most kFfdMaxScanBlocks (its kept list is staged in LDS).
-#ifndef FFD_SCAN_WGS
-#define FFD_SCAN_WGS 1024
-#endif
-constexpr int kScanWorkgroups = FFD_SCAN_WGS;
+// Workgroups of the scan kernel per (sequence, KV head): about kScanWorkgroups in all (one 8-wave
+// workgroup per CU: 8 waves x 4 blocks of 2 KiB in flight cover a CU's share of the HBM bandwidth at
+// its load latency; 512 or 1024 workgroups of 8 or 4 waves measured 0.6-1.1 us slower at 4 x 128K),
+// each scanning at least kMinScanBlocks blocks so the pseudo-max and query setup stay a small part
+// of its work, and at most kFfdMaxScanBlocks (their maxima are staged in LDS).
+constexpr int kScanWorkgroups = 256;
 constexpr int kMinScanBlocks = 16;
 
 int scan_splits(int B, int Hkv, int Lcap) {
@@ -139,11 +138,11 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
 template <int NT, int BITS>
 void launch_scan_nt(int mode, dim3 grid, hipStream_t stream, const ScanArgs& sa) {
     if (mode == kSelRefinedPM)
-        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelRefinedPM>), grid, dim3(kThreads), 0, stream, sa);
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelRefinedPM>), grid, dim3(kScanThreads), 0, stream, sa);
     else if (mode == kSelTopK)
-        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelTopK>), grid, dim3(kThreads), 0, stream, sa);
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelTopK>), grid, dim3(kScanThreads), 0, stream, sa);
     else
-        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelThumbnailPM>), grid, dim3(kThreads), 0, stream, sa);
+        hipLaunchKernelGGL((ffd_scan_kernel<NT, BITS, kSelThumbnailPM>), grid, dim3(kScanThreads), 0, stream, sa);
 }
 
 template <int BITS>

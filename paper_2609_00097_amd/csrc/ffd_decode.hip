@@ -51,7 +51,6 @@ namespace {
 #define FFD_REFINE_OCC 3
 #endif
 constexpr int kRing2 = FFD_SCAN_RING;         // 2-bit scan loads in flight per wave (blocks)
-constexpr int kPMW2 = 2;                      // 2-bit pseudo-max window blocks per wave per pass
 constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
 constexpr int kChunk = kFfdChunk;             // list entries staged per pass of the refinement kernel
 
@@ -178,6 +177,25 @@ __device__ __forceinline__ BlockScan<BITS> load_block_scan(const uint32_t* __res
     return r;
 }
 
+// The same loads through buffer resources whose ranges end at a workgroup's last block: a block
+// index at or past that end reads zeros without touching memory (the hardware range check of a raw
+// buffer), so a wave may request blocks that turn out not to exist.
+constexpr int kRawBufferWord3 = 0x00020000;    // gfx9 raw buffer: 32-bit data format, no swizzle
+template <int BITS>
+__device__ __forceinline__ BlockScan<BITS> load_block_scan_rsrc(__amdgpu_buffer_rsrc_t rc, __amdgpu_buffer_rsrc_t ra,
+                                                                int j, int lane) {
+    BlockScan<BITS> r;
+    const uint32_t base = ((uint32_t)j * 64u + (uint32_t)lane) * (16u * BITS);
+#pragma unroll
+    for (int i = 0; i < BITS; ++i) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rc, (int)(base + 16u * i), 0, 0);
+        r.w[i] = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+    const auto m = __builtin_amdgcn_raw_buffer_load_b64(ra, (int)((uint32_t)j * 128u + (uint32_t)(lane & 15) * 8u), 0, 0);
+    r.mm = make_uint2(m[0], m[1]);
+    return r;
+}
+
 // Thumbnail scores of one 16-token tile for this lane's head(s) and token n: tw holds the lane's b
 // words of the tile (64-dim chunk 0, then chunk 1), M the token's absmax; -inf for a token past L.
 template <int NT, int BITS>
@@ -231,9 +249,10 @@ __device__ __forceinline__ void block_scores(const BlockScan<BITS>& ld, int j, i
 template <int NT>
 struct ScanLds {
     QueryLds<NT> qs;
-    alignas(16) float pm[kWaves][4 * NT];                 // each wave's window maxima per head
+    alignas(16) float pm[kScanWaves][4 * NT];             // each wave's window maxima per head
     alignas(16) float sig[kFfdMaxScanBlocks][4 * NT];     // block maxima of the thumbnail scores per head
-    int nkept[kWaves];                        // kept blocks per wave
+    int nkept[kScanWaves];                    // kept blocks per wave
+    int next;                                 // next block to hand out
 };
 
 // ---- refinement helpers ---------------------------------------------------------------------
@@ -300,14 +319,12 @@ struct RefineLds {
 // ================================================================================================
 // Scan: b-bit thumbnail scan and pseudo-max, then the keep decisions; the kept list (or, for the
 // top-k rule, every block's scores) to the workspace.
-// Grid (S1, Hkv, B); workgroup s1 scans blocks [s1 * bps, (s1 + 1) * bps) of one (sequence, KV
-// head), bps = ceil(nblk / S1) <= kFfdMaxScanBlocks; wave w takes a contiguous quarter of them and
-// keeps kRing blocks in flight.
+// Grid (S1, Hkv, B) of kScanWaves-wave workgroups; workgroup s1 scans blocks [s1 * bps, (s1 + 1) *
+// bps) of one (sequence, KV head), bps = ceil(nblk / S1) <= kFfdMaxScanBlocks; its waves take the
+// blocks one at a time from an LDS counter and keep kRing blocks in flight each.
 // ================================================================================================
-// Loads in flight per wave: a ring of blocks and the pseudo-max window blocks of a pass, fewer for the
-// wider thumbnails (whose blocks are 2x and 4x larger).
+// Blocks in flight per wave, fewer for the wider thumbnails (whose blocks are 2x and 4x larger).
 template <int BITS> constexpr int scan_ring() { return BITS == 2 ? kRing2 : 2; }
-template <int BITS> constexpr int scan_pmw() { return BITS == 8 ? 1 : kPMW2; }
 
 // Adds the residual term of Eq. 4 to the thumbnail scores sc of block j (the refined logits of its
 // tokens, computed exactly as the refinement kernel computes them).
@@ -336,17 +353,14 @@ __device__ __forceinline__ void add_residual_term(const int8_t* __restrict__ res
     }
 }
 
-// Workgroups per CU (a lower bound that caps registers at 512 / (4 n) per lane): the 8-bit blocks,
-// and for eight heads the 4-bit blocks or the refined pseudo-max's residual tiles, need more registers.
-template <int NT, int BITS, int MODE> constexpr int scan_occupancy() {
-    return BITS == 8 ? 2 : (NT == 2 && (BITS == 4 || MODE == kSelRefinedPM) ? 3 : 4);
-}
+// Workgroups per CU the registers must allow: two, so that a grid slightly larger than the CU count
+// (S1 rounded up) runs in one wave of workgroups; the 8-bit blocks need more registers.
+template <int BITS> constexpr int scan_occupancy() { return BITS == 8 ? 1 : 2; }
 
 template <int NT, int BITS, int MODE>
-__global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void ffd_scan_kernel(ScanArgs a) {
+__global__ __launch_bounds__(kScanThreads, scan_occupancy<BITS>()) void ffd_scan_kernel(ScanArgs a) {
     constexpr bool kTopK = MODE == kSelTopK;
     constexpr int kRing = scan_ring<BITS>();
-    constexpr int kPMW = scan_pmw<BITS>();
     __shared__ ScanLds<NT> sm;
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -369,17 +383,26 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * BITS);
     const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
 
-    // This wave's blocks: [jw0, jw0 + nbw).
-    const int qw_blocks = (bps + kWaves - 1) / kWaves;
-    const int jw0 = min(jb + wave * qw_blocks, je);
-    const int nbw = min(jw0 + qw_blocks, je) - jw0;
-    const int jclamp = nbw > 0 ? jw0 + nbw - 1 : max(je - 1, 0);   // block 0 always exists
+    // The stream reads through buffer resources whose ranges end at block je, so a request for a
+    // block >= je reads zeros without touching memory (the hardware range check of a raw buffer):
+    // every load is issued unconditionally, and uniform control flow lets the compiler wait for
+    // exactly the load it needs instead of draining every load in flight (which a conditional load
+    // made it do). Offsets and sizes are unsigned 32-bit: at most 2^18 blocks of 8 KiB.
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(codes_bh), (short)0, (int)((uint32_t)je * (1024u * BITS)), kRawBufferWord3);
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(absmax_bh), (short)0, (int)((uint32_t)je * 128u), kRawBufferWord3);
+    // Work distribution: wave w starts with blocks jb + kRing w + r (r < kRing), then takes the next
+    // block from an LDS counter each time it scores one, so the waves of a CU finish together however
+    // its memory requests are served (a CU serves its oldest waves first: with fixed shares, the
+    // workgroups of one CU ended up to 12 us apart at 4 x 128K).
+    int js[kRing];                                  // block held by each ring slot (>= je: none)
+#pragma unroll
+    for (int r = 0; r < kRing; ++r) js[r] = jb + kRing * wave + r;
 
-    // Loads are issued unconditionally (out-of-range indices are clamped to valid data that is then
-    // ignored): uniform control flow lets the compiler wait for exactly the load it needs instead of
-    // draining every load in flight. Order: queries, the window blocks of the first pseudo-max pass,
-    // the first ring round. Each wave scores its window blocks on its own before its first block
-    // (the refined logits: after the stream, with the window blocks' residual tiles) and only
+    // Order of requests: queries, the window blocks of the first pseudo-max pass (clamped to valid
+    // blocks), the first ring round. Each wave scores its window blocks on its own before its first
+    // block (the refined logits: after the stream, with the window blocks' residual tiles) and only
     // writes their maxima to LDS; every keep decision waits for the end of the stream, where the
     // pseudo-max is known, so no wave waits on another before or during its stream (a
     // workgroup-wide window pass before the stream held every wave until the slowest one's window
@@ -396,16 +419,14 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
     auto win_block = [&](int idx) { return min(pm_block(min(idx, max(npm, 1) - 1)), jlast); };
     constexpr bool kEarlyWindows = MODE == kSelThumbnailPM;
-    BlockScan<BITS> win[kPMW];
-    auto load_windows = [&](int base) {
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i) win[i] = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + kWaves * i + wave), lane);
-    };
-    if constexpr (kEarlyWindows) load_windows(0);
+    BlockScan<BITS> win;                            // wave w's window block of the current pass
+    auto load_window = [&](int base) { win = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + wave), lane); };
+    if constexpr (kEarlyWindows) load_window(0);
     BlockScan<BITS> ring[kRing];
 #pragma unroll
-    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan<BITS>(codes_bh, absmax_bh, min(jw0 + i, jclamp), lane);
-    if constexpr (MODE == kSelRefinedPM) load_windows(0);
+    for (int i = 0; i < kRing; ++i) ring[i] = load_block_scan_rsrc<BITS>(rc, ra, min(js[i], je), lane);
+    if (tid == 0) sm.next = jb + kScanWaves * kRing;   // visible after the barriers below
+    if constexpr (MODE == kSelRefinedPM) load_window(0);
 
     HeadConsts<NT> hc;
     build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
@@ -423,18 +444,15 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
             for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
         }
     };
-    auto window_pass = [&](const BlockScan<BITS> (&wb)[kPMW], int base) {
-#pragma unroll
-        for (int i = 0; i < kPMW; ++i) {
-            const int idx = base + kWaves * i + wave;
-            if (idx >= npm) continue;                   // wave-uniform
-            const int j = pm_block(idx);
-            float sc[NT][4];
-            block_scores<NT, BITS>(wb[i], j, lane, L, hc, sc);
-            if constexpr (MODE == kSelRefinedPM)
-                add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, wb[i].mm, j, lane, hc, sc);
-            window_max(sc, j);
-        }
+    auto window_pass = [&](int base) {              // wave w: window block base + w
+        const int idx = base + wave;
+        if (idx >= npm) return;                     // wave-uniform
+        const int j = pm_block(idx);
+        float sc[NT][4];
+        block_scores<NT, BITS>(win, j, lane, L, hc, sc);
+        if constexpr (MODE == kSelRefinedPM)
+            add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win.mm, j, lane, hc, sc);
+        window_max(sc, j);
     };
     auto consume = [&](const BlockScan<BITS>& blk, int j) {
         float sc[NT][4];
@@ -450,32 +468,32 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
             }
         }
     };
-    // Every round but the last refills each slot with the block kRing ahead (clamped to the wave's
-    // own last block, which is then still cached); the last round issues no loads, so no wave waits
-    // on a load it does not use.
-    auto ring_round = [&](int i) {
+    if constexpr (kEarlyWindows) window_pass(0);     // its block arrives ahead of the first round
+    // Each slot in turn: take the next block number (its LDS round trip hides behind the scoring),
+    // score the slot's block if it has one, refill the slot. The loop ends once a whole round has
+    // taken no block below je: every slot then holds none, and its last loads read no memory.
+    for (bool more = true; more;) {                 // wave-uniform
+        more = false;
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
-            const int j = jw0 + i + r;
-            consume(ring[r], j);
-            ring[r] = load_block_scan<BITS>(codes_bh, absmax_bh, min(j + kRing, jclamp), lane);
+            int jn = 0;
+            if (lane == 0) jn = atomicAdd(&sm.next, 1);
+            jn = __builtin_amdgcn_readfirstlane(jn);
+            if (js[r] < je) consume(ring[r], js[r]);
+            ring[r] = load_block_scan_rsrc<BITS>(rc, ra, min(jn, je), lane);
+            js[r] = jn;
+            more |= jn < je;
         }
-    };
-    if constexpr (kEarlyWindows) window_pass(win, 0);   // its blocks arrive ahead of the first round
-    int i0 = 0;
-    for (; i0 + kRing < nbw; i0 += kRing) ring_round(i0);
-#pragma unroll
-    for (int r = 0; r < kRing; ++r)
-        if (i0 + r < nbw) consume(ring[r], jw0 + i0 + r);
+    }
 
     if constexpr (kTopK) return;                // the top-k rule compares block scores with each other
 
     // ---- pseudo-max over the sink and local windows (Eq. 3): the first pass unless done during
     // the stream, further passes (wide windows) loaded now -------------------------------------
-    if constexpr (!kEarlyWindows) window_pass(win, 0);
-    for (int base = kWaves * kPMW; base < npm; base += kWaves * kPMW) {
-        load_windows(base);
-        window_pass(win, base);
+    if constexpr (!kEarlyWindows) window_pass(0);
+    for (int base = kScanWaves; base < npm; base += kScanWaves) {
+        load_window(base);
+        window_pass(base);
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -491,7 +509,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     for (int t = 0; t < NT; ++t) {
         float4 m = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
+        for (int w = 0; w < kScanWaves; ++w) {
             const float4 p = reinterpret_cast<const float4*>(sm.pm[w])[t];
             m.x = fmaxf(m.x, p.x); m.y = fmaxf(m.y, p.y); m.z = fmaxf(m.z, p.z); m.w = fmaxf(m.w, p.w);
         }
@@ -503,13 +521,14 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     if (a.m_tilde && s == 0 && tid < G) {
         float m = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sm.pm[w][tid]);
+        for (int w = 0; w < kScanWaves; ++w) m = fmaxf(m, sm.pm[w][tid]);
         a.m_tilde[(size_t)b * a.Hq + hq0 + tid] = m;
     }
-    // lane i of wave w decides the wave's block jw0 + i (a wave holds at most 64 blocks)
+    // lane i of wave w decides block jb + 64 w + i (bps <= kFfdMaxScanBlocks <= 64 kScanWaves)
+    static_assert(kFfdMaxScanBlocks <= 64 * kScanWaves, "one decision per lane");
     uint32_t bits = 0;
-    const int jl = jw0 + lane;
-    if (lane < nbw) {
+    const int jl = jb + 64 * wave + lane;
+    if (jl < je) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const float4 sg = reinterpret_cast<const float4*>(sm.sig[jl - jb])[t];
@@ -526,7 +545,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
     __syncthreads();
     int before = 0, total = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < kScanWaves; ++w) {
         const int c = sm.nkept[w];
         before += w < wave ? c : 0;
         total += c;
@@ -536,7 +555,7 @@ __global__ __launch_bounds__(kThreads, (scan_occupancy<NT, BITS, MODE>())) void 
 
     // Mask entries past the end of the sequence are zero (spread over the scan workgroups).
     if (a.mask) {
-        for (int j = nblk + s * kThreads + tid; j < nblk_cap; j += a.S1 * kThreads)
+        for (int j = nblk + s * kScanThreads + tid; j < nblk_cap; j += a.S1 * kScanThreads)
             for (int h = 0; h < G; ++h) a.mask[((size_t)b * a.Hq + hq0 + h) * nblk_cap + j] = 0;
     }
 }

@@ -11,6 +11,8 @@ constexpr int kFfdChunk = 1024;
 // Most blocks one scan workgroup covers (its kept list is staged in LDS), most scan workgroups per
 // (sequence, KV head).
 constexpr int kFfdMaxScanBlocks = 256;
+constexpr int kScanWaves = 8;                  // waves per scan workgroup (one workgroup per CU)
+constexpr int kScanThreads = 64 * kScanWaves;
 constexpr int kFfdMaxScanSplits = 1024;
 
 // Thumbnail depth b (App. C: 2+8, 4+8, 8+8): 2^b levels c - Lv, Lv = (2^b - 1) / 2; a token's codes

@@ -48,11 +48,11 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
     # partials (S*P + P)*G*(D+2)*4 | table P*8 | counts P*S1*4 | lists P*C*4 | block scores P*C*G*4,
-    # each region on a 256-byte boundary (S1 = 32 scan splits at 4 x 8 x 128K, 4 at 1 x 2 x 4K)
+    # each region on a 256-byte boundary (S1 = 8 scan splits at 4 x 8 x 128K, 4 at 1 x 2 x 4K)
     up = lambda x: -(-x // 256) * 256
     P, G, C = 32, 4, 2048
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
-        up((15 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 32 * 4) + up(P * C * 4)
+        up((15 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
         + P * C * G * 4)
     P, G, C = 2, 8, 64
     assert so.ffd_workspace_bytes(1, 16, 2, 4096, 128, 3) == (
