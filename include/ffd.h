@@ -36,11 +36,14 @@
  * cache (ffd_quantize_keys, ffd_append_kv) and to read it (ffd_decode_attention).
  *
  * Quantized-key storage (this library's format; the paper fixes none). Per (b, kvh):
- *  - codes  uint32 [Lcap/64][64][4b]: block j = tokens 64j..64j+63; lane l = n + 16g holds, for
- *           token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims 64cc + 16g + e, e = 4k + i,
- *           in the b/2 words from (2*t4 + cc) * b/2: dim e in word (2*t4 + cc) * b/2 + k / (8/b) at
- *           bit 8i + b * (k % (8/b)). The field holds c for b = 2, 4 and the byte c - 128 (two's
- *           complement) for b = 8. For b = 2: word 2*t4 + cc, bit 8i + 2k.
+ *  - codes  uint32 [Lcap/64][b][64][4]: block j = tokens 64j..64j+63 holds 4b words for each lane
+ *           l = n + 16g, word w of lane l at element [j][w / 4][l][w % 4] (so each group of four
+ *           words is 1 KiB contiguous over the 64 lanes, one coalesced 16-byte load per lane). Lane
+ *           l's words hold, for token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims
+ *           64cc + 16g + e, e = 4k + i, in the b/2 words from (2*t4 + cc) * b/2: dim e in word
+ *           (2*t4 + cc) * b/2 + k / (8/b) at bit 8i + b * (k % (8/b)). The field holds c for
+ *           b = 2, 4 and the byte c - 128 (two's complement) for b = 8. For b = 2: word 2*t4 + cc,
+ *           bit 8i + 2k.
  *  - absmax bf16 [Lcap/64][16][4]: element [j][n][t4] = M = max_i |k_i| of token 64j + 16*t4 + n.
  *  - resid  int8 [Lcap/16][2][64][16]: element [T][cc][n + 16g][e] is the residual of token 16T + n
  *           at dim 64cc + 16g + e.

@@ -423,8 +423,9 @@ def near_threshold(sigma, m_tilde, delta, band=1e-3):
 # Storage layouts of the quantized copy (this implementation's format; the paper fixes none).
 # They are written out independently of the HIP code, from the format's definition:
 #
-#  codes  uint32 [B, Hkv, Lcap/64, 64, 4b] for a b-bit thumbnail. In block j (tokens 64j..64j+63),
-#         lane l = n + 16g holds, for token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims
+#  codes  uint32 [B, Hkv, Lcap/64, b, 64, 4] for a b-bit thumbnail. Block j (tokens 64j..64j+63)
+#         holds 4b words for each lane l = n + 16g; word w of lane l is element [j, w // 4, l, w % 4].
+#         Lane l's words hold, for token 64j + 16*t4 + n and 64-dim chunk cc, the codes of dims
 #         64cc + 16g + e (e = 4k + i, k, i in 0..3) in the b/2 words starting at (2*t4 + cc) * b/2:
 #         dim e sits in word (2*t4 + cc) * b/2 + k // (8/b), at bit 8i + b * (k % (8/b)). The field
 #         holds c for b = 2, 4 and the byte c - 128 (two's complement) for b = 8. For b = 2 this is
@@ -440,10 +441,10 @@ def _code_field(c: int, bits: int) -> int:
 
 
 def pack_codes(codes: np.ndarray, bits: int = 2) -> np.ndarray:
-    """Pack ``codes [Lcap, 128]`` (``0 .. 2^b - 1``) into the ``[Lcap/64, 64, 4b]`` uint32 layout."""
+    """Pack ``codes [Lcap, 128]`` (``0 .. 2^b - 1``) into the ``[Lcap/64, b, 64, 4]`` uint32 layout."""
     Lcap = codes.shape[0]
     per = 8 // bits                                   # codes per byte
-    out = np.zeros((Lcap // 64, 64, 4 * bits), dtype=np.uint32)
+    out = np.zeros((Lcap // 64, bits, 64, 4), dtype=np.uint32)
     for j in range(Lcap // 64):
         for g in range(4):
             for n in range(16):
@@ -455,13 +456,13 @@ def pack_codes(codes: np.ndarray, bits: int = 2) -> np.ndarray:
                             k, i = divmod(e, 4)
                             w = w0 + k // per
                             f = _code_field(codes[t, 64 * cc + 16 * g + e], bits)
-                            out[j, n + 16 * g, w] |= np.uint32(f << (8 * i + bits * (k % per)))
+                            out[j, w // 4, n + 16 * g, w % 4] |= np.uint32(f << (8 * i + bits * (k % per)))
     return out
 
 
 def unpack_codes(packed: np.ndarray, Lcap: int, bits: int = 2) -> np.ndarray:
     """Inverse of :func:`pack_codes`."""
-    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 64, 64, 4 * bits)
+    packed = np.asarray(packed, dtype=np.uint32).reshape(Lcap // 64, bits, 64, 4)
     per = 8 // bits
     codes = np.zeros((Lcap, 128), dtype=np.int64)
     for j in range(Lcap // 64):
@@ -472,7 +473,8 @@ def unpack_codes(packed: np.ndarray, Lcap: int, bits: int = 2) -> np.ndarray:
                         w0 = (2 * t4 + cc) * (bits // 2)
                         for e in range(16):
                             k, i = divmod(e, 4)
-                            word = int(packed[j, n + 16 * g, w0 + k // per])
+                            w = w0 + k // per
+                            word = int(packed[j, w // 4, n + 16 * g, w % 4])
                             f = (word >> (8 * i + bits * (k % per))) & (2 ** bits - 1)
                             c = (f + 128) & 0xFF if bits == 8 else f
                             codes[64 * j + 16 * t4 + n, 64 * cc + 16 * g + e] = c
@@ -490,7 +492,19 @@ def pack_codes_fast(codes: np.ndarray, bits: int = 2) -> np.ndarray:
     f = f.transpose(0, 4, 2, 1, 3, 5, 6, 7)           # j, g, n, t4, cc, k // per, k % per, i
     shift = (8 * np.arange(4)[None, :] + bits * np.arange(per)[:, None]).astype(np.uint32)
     words = np.bitwise_or.reduce((f << shift).reshape(*f.shape[:6], 4 * per), axis=-1)
-    return words.reshape(Lcap // 64, 64, 4 * bits).astype(np.uint32)
+    return piece_major(words.reshape(Lcap // 64, 64, 4 * bits).astype(np.uint32), bits)
+
+
+def piece_major(lane_words: np.ndarray, bits: int) -> np.ndarray:
+    """``[J, 64, 4b]`` (lane, word) -> the stored ``[J, b, 64, 4]`` order (word w at [w // 4, l, w % 4])."""
+    J = lane_words.shape[0]
+    return np.ascontiguousarray(lane_words.reshape(J, 64, bits, 4).transpose(0, 2, 1, 3))
+
+
+def lane_words(packed: np.ndarray, bits: int) -> np.ndarray:
+    """Inverse of :func:`piece_major`."""
+    J = packed.shape[0]
+    return np.ascontiguousarray(packed.reshape(J, bits, 64, 4).transpose(0, 2, 1, 3)).reshape(J, 64, 4 * bits)
 
 
 def pack_absmax(M_bits: np.ndarray) -> np.ndarray:
@@ -514,7 +528,7 @@ def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = Non
     """
     B, Hkv, Lcap, d = k_bits.shape
     t_end = Lcap if t_end is None else t_end
-    codes = np.zeros((B, Hkv, Lcap // 64, 64, 4 * bits), dtype=np.uint32)
+    codes = np.zeros((B, Hkv, Lcap // 64, bits, 64, 4), dtype=np.uint32)
     absmax = np.zeros((B, Hkv, Lcap // 64, 16, 4), dtype=np.uint16)
     resid = np.zeros((B, Hkv, Lcap // 16, 2, 64, 16), dtype=np.int8)
     live = np.zeros(Lcap, dtype=bool)
@@ -529,9 +543,9 @@ def quantize_cache(k_bits: np.ndarray, t_begin: int = 0, t_end: int | None = Non
             packed = pack_codes_fast(c, bits)
             if bits == 8:                             # tokens outside the range hold zero words
                 dead = ~live.reshape(Lcap // 64, 4, 16).transpose(0, 2, 1)   # j, n, t4
-                packed = packed.reshape(Lcap // 64, 4, 16, 4, 2, 4)          # j, g, n, t4, cc, k
-                packed[np.broadcast_to(dead[:, None, :, :, None, None], packed.shape)] = 0
-                packed = packed.reshape(Lcap // 64, 64, 32)
+                lw = lane_words(packed, bits).reshape(Lcap // 64, 4, 16, 4, 2, 4)   # j, g, n, t4, cc, k
+                lw[np.broadcast_to(dead[:, None, :, :, None, None], lw.shape)] = 0
+                packed = piece_major(lw.reshape(Lcap // 64, 64, 32), bits)
             codes[b, h] = packed
             absmax[b, h] = pack_absmax(Mb)
             resid[b, h] = pack_resid(r)

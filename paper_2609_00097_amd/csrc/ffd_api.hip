@@ -109,7 +109,7 @@ FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
     w.rows = ((size_t)S * pairs + pairs) * (size_t)(Hq / Hkv);
     w.table_off = round_up(w.rows * (D + 2) * sizeof(float), kAlign);
     w.counts_off = w.table_off + round_up(pairs * 2 * sizeof(int), kAlign);
-    w.lists_off = w.counts_off + round_up(pairs * scan_splits(B, Hkv, Lcap) * sizeof(int), kAlign);
+    w.lists_off = w.counts_off + round_up(pairs * (size_t)scan_splits(B, Hkv, Lcap) * sizeof(int), kAlign);
     w.sigma_off = w.lists_off + round_up(pairs * nblk_cap * sizeof(uint32_t), kAlign);
     w.total = w.sigma_off + pairs * nblk_cap * (size_t)(Hq / Hkv) * sizeof(float);
     return w;

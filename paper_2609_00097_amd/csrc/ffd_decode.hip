@@ -157,8 +157,9 @@ __device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint3
     }
 }
 
-// One lane's share of a block's thumbnail: 16b bytes of codes (both 64-dim halves of its token in
-// each of the four tiles) and the absmax of its four tokens.
+// One lane's share of a block's thumbnail: its 4b code words (both 64-dim halves of its token in
+// each of the four tiles; w[i] = words 4i .. 4i + 3, each load 1 KiB contiguous over the wave) and
+// the absmax of its four tokens.
 template <int BITS>
 struct BlockScan {
     uint4 w[BITS];
@@ -169,10 +170,10 @@ template <int BITS>
 __device__ __forceinline__ BlockScan<BITS> load_block_scan(const uint32_t* __restrict__ codes_bh,
                                                            const uint16_t* __restrict__ absmax_bh, int j,
                                                            int lane) {
-    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + ((size_t)j * 64 + lane) * BITS;
+    const uint4* cp = reinterpret_cast<const uint4*>(codes_bh) + (size_t)j * 64 * BITS + lane;
     BlockScan<BITS> r;
 #pragma unroll
-    for (int i = 0; i < BITS; ++i) r.w[i] = cp[i];
+    for (int i = 0; i < BITS; ++i) r.w[i] = cp[64 * i];               // words 4i .. 4i + 3
     r.mm = *reinterpret_cast<const uint2*>(absmax_bh + (size_t)j * 64 + (lane & 15) * 4);
     return r;
 }
@@ -185,10 +186,10 @@ template <int BITS>
 __device__ __forceinline__ BlockScan<BITS> load_block_scan_rsrc(__amdgpu_buffer_rsrc_t rc, __amdgpu_buffer_rsrc_t ra,
                                                                 int j, int lane) {
     BlockScan<BITS> r;
-    const uint32_t base = ((uint32_t)j * 64u + (uint32_t)lane) * (16u * BITS);
+    const uint32_t base = (uint32_t)j * (1024u * BITS) + (uint32_t)lane * 16u;
 #pragma unroll
     for (int i = 0; i < BITS; ++i) {
-        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rc, (int)(base + 16u * i), 0, 0);
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rc, (int)(base + 1024u * i), 0, 0);
         r.w[i] = make_uint4(v[0], v[1], v[2], v[3]);
     }
     const auto m = __builtin_amdgcn_raw_buffer_load_b64(ra, (int)((uint32_t)j * 128u + (uint32_t)(lane & 15) * 8u), 0, 0);
@@ -280,15 +281,15 @@ __device__ __forceinline__ RefineTile<NT, RBITS> load_refine_tile(const int8_t* 
     r.r0 = rp[0];
     r.r1 = rp[64];
     r.vt = load_vtile(v_bh, 16 * tile, last_row, lane);
-    // the lane's 4b words of block j; tile T4 is words T4*b .. T4*b + b - 1
-    const uint32_t* cp = codes_bh + ((size_t)j * 64 + lane) * (4 * RBITS) + T4 * RBITS;
+    // tile T4 is the lane's words T4*b .. T4*b + b - 1 of block j; word w at [w / 4][lane][w % 4]
+    const uint32_t* cb = codes_bh + (size_t)j * (256 * RBITS) + lane * 4;
     if constexpr (RBITS == 2) {
-        const uint2 w = *reinterpret_cast<const uint2*>(cp);
+        const uint2 w = *reinterpret_cast<const uint2*>(cb + (T4 >> 1) * 256 + 2 * (T4 & 1));
         r.cw[0] = w.x; r.cw[1] = w.y;
     } else {
 #pragma unroll
         for (int i = 0; i < RBITS / 4; ++i) {
-            const uint4 w = reinterpret_cast<const uint4*>(cp)[i];
+            const uint4 w = *reinterpret_cast<const uint4*>(cb + (T4 * (RBITS / 4) + i) * 256);
             r.cw[4 * i] = w.x; r.cw[4 * i + 1] = w.y; r.cw[4 * i + 2] = w.z; r.cw[4 * i + 3] = w.w;
         }
     }

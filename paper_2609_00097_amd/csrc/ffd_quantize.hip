@@ -119,21 +119,23 @@ __device__ __forceinline__ QuantToken<BITS> quantize_token(uint4 raw, int j16) {
 }
 
 // Store token t of (b, kvh) = row bh into the codes / absmax / residual layouts (lane j16's share).
-// Codes: lane n16 + 16g of block t/64 holds the (t4, cc) group's b/2 words from (2 t4 + cc) b/2.
+// Codes: lane l = n16 + 16g of block t/64 holds the (t4, cc) group's b/2 words from (2 t4 + cc) b/2;
+// its word w sits at [w / 4][l][w % 4] of the block's 4b x 64 words.
 template <int BITS>
 __device__ __forceinline__ void store_token(const QuantToken<BITS>& qt, int j16, size_t bh, int t, int Lcap,
                                             uint32_t* codes, uint16_t* absmax, int8_t* resid) {
     const int n16 = t & 15, t4 = (t >> 4) & 3;
     const int w16 = j16 >> 1;                              // 16-dim group 0..7
     const int cc = w16 >> 2, g = w16 & 3;
-    uint32_t* row = codes + ((bh * (size_t)(Lcap / 64) + (t >> 6)) * 64 + n16 + 16 * g) * (4 * BITS) +
-                    (2 * t4 + cc) * (BITS / 2);
+    const int w = (2 * t4 + cc) * (BITS / 2) + (BITS == 2 ? 0 : (BITS / 4) * (j16 & 1));   // first word
+    uint32_t* dst = codes + (bh * (size_t)(Lcap / 64) + (t >> 6)) * (64 * 4 * BITS) + (w >> 2) * 256 +
+                    (n16 + 16 * g) * 4 + (w & 3);
     if constexpr (BITS == 2) {
-        if ((j16 & 1) == 0) row[0] = qt.word[0];
+        if ((j16 & 1) == 0) dst[0] = qt.word[0];
     } else if constexpr (BITS == 4) {
-        row[j16 & 1] = qt.word[0];
+        dst[0] = qt.word[0];
     } else {
-        *reinterpret_cast<uint2*>(row + 2 * (j16 & 1)) = make_uint2(qt.word[0], qt.word[1]);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(qt.word[0], qt.word[1]);   // words w, w + 1 (w even)
     }
     {
         const int rc = j16 >> 3, rg = (j16 & 7) >> 1, e0 = 8 * (j16 & 1);

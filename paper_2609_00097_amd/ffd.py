@@ -126,15 +126,15 @@ def new_workspace(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0, dev
 def quantized_shapes(B: int, Hkv: int, Lcap: int, bits: int = 2):
     """Shapes of (codes int32, absmax bf16, resid int8) for a cache of capacity Lcap with a
     ``bits``-bit thumbnail."""
-    return ((B, Hkv, Lcap // 64, 64, 4 * bits), (B, Hkv, Lcap // 64, 16, 4),
+    return ((B, Hkv, Lcap // 64, bits, 64, 4), (B, Hkv, Lcap // 64, 16, 4),
             (B, Hkv, Lcap // 16, 2, 64, 16))
 
 
 def thumb_bits(codes: torch.Tensor) -> int:
-    """The thumbnail depth of a codes tensor, from its last dimension (4 words per bit)."""
-    bits = codes.shape[-1] // 4 if codes.dim() == 5 else 0
-    if bits not in THUMB_BITS or codes.shape[-1] != 4 * bits:
-        raise ValueError(f"codes must be [B, Hkv, Lcap/64, 64, 4b] with b in {THUMB_BITS}, "
+    """The thumbnail depth of a codes tensor ``[B, Hkv, Lcap/64, b, 64, 4]``."""
+    bits = codes.shape[-3] if codes.dim() == 6 and tuple(codes.shape[-2:]) == (64, 4) else 0
+    if bits not in THUMB_BITS:
+        raise ValueError(f"codes must be [B, Hkv, Lcap/64, b, 64, 4] with b in {THUMB_BITS}, "
                          f"got {tuple(codes.shape)}")
     return bits
 

@@ -103,9 +103,9 @@ def test_codes_shape_names_the_depth():
     c = I.small_case(seed=5, B=1, Hq=8, Hkv=2, seq_lens=(100,))
     up = Uploaded(c)
     codes, absmax, resid = ffd.quantize_keys(up.k, bits=4)
-    assert codes.shape[-1] == 16
+    assert codes.shape[-3:] == (4, 64, 4)
     with pytest.raises(ValueError):
-        ffd.decode_attention(up.q, codes[..., :12].contiguous(), absmax, resid, up.v, up.seq_lens,
+        ffd.decode_attention(up.q, codes[..., :3, :, :].contiguous(), absmax, resid, up.v, up.seq_lens,
                              delta=5.0)
     with pytest.raises(ValueError):
         ffd.quantize_keys(up.k, bits=3)

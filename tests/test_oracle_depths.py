@@ -44,8 +44,8 @@ def test_worked_examples_match_hand_computation():
             vec[0, 8] = case["M"]
             c, _, _ = O.quantize_keys(vec, b)
             p = O.pack_codes(c, b)
-            # token 0, dims 0..7: lane 0, words 0 and 1, byte i of word k is dim 4k + i
-            got = [int(np.int8(np.uint8((int(p[0, 0, e // 4]) >> (8 * (e % 4))) & 0xFF))) for e in range(8)]
+            # token 0, dims 0..7: lane 0, words 0 and 1 (stored at [0, 0, 0, w]), byte i of word k is dim 4k + i
+            got = [int(np.int8(np.uint8((int(p[0, 0, 0, e // 4]) >> (8 * (e % 4))) & 0xFF))) for e in range(8)]
             assert got == case["stored_bytes"]
 
 
@@ -192,19 +192,19 @@ def test_infinite_delta_equals_dense_attention_on_reconstructed_keys(bits):
 @pytest.mark.parametrize("bits", WIDE)
 def test_pack_codes_single_token_hand_checked(bits):
     """Token 81 = block 1, t4 = 1, n = 1; dim 16 + 5 = cc 0, g 1, e 5 (k 1, i 1) -> lane 17.
-    4-bit: word (2*1 + 0)*2 + 1//2 = 4, bit 8 + 4*(1%2) = 12. 8-bit: word (2*1 + 0)*4 + 1 = 9,
-    bit 8, holding the byte c - 128."""
+    4-bit: word (2*1 + 0)*2 + 1//2 = 4 (stored at [1, 1, 17, 0]), bit 8 + 4*(1%2) = 12. 8-bit: word
+    (2*1 + 0)*4 + 1 = 9 (stored at [1, 2, 17, 1]), bit 8, holding the byte c - 128."""
     codes = np.zeros((128, 128), dtype=np.int64)
     c = 13 if bits == 4 else 200
     codes[81, 16 + 5] = c
     p = O.pack_codes(codes, bits)
     if bits == 4:
         nz = np.argwhere(p)
-        assert nz.tolist() == [[1, 17, 4]] and int(p[1, 17, 4]) == 13 << 12
+        assert nz.tolist() == [[1, 1, 17, 0]] and int(p[1, 1, 17, 0]) == 13 << 12
     else:
         # every other code is 0 -> byte 0x80; the one entry holds 200 - 128 = 72
-        assert (int(p[1, 17, 9]) >> 8) & 0xFF == 72
-        assert int(p[1, 17, 9]) & 0xFFFF00FF == 0x80800080
+        assert (int(p[1, 2, 17, 1]) >> 8) & 0xFF == 72
+        assert int(p[1, 2, 17, 1]) & 0xFFFF00FF == 0x80800080
         assert np.count_nonzero(p != 0x80808080) == 1
 
 
@@ -223,12 +223,12 @@ def test_quantize_cache_range_only_defines_live_tokens(bits):
     c = small_case(seed=3, B=1, Hq=4, Hkv=1, seq_lens=(128,))
     codes, absmax, resid = O.quantize_cache(c.k, 32, 96, bits)
     full = O.quantize_cache(c.k, bits=bits)
-    assert codes.shape[-1] == 4 * bits
+    assert codes.shape[-3:] == (bits, 64, 4)
     cu = O.unpack_codes(codes[0, 0], 128, bits)
     cf = O.unpack_codes(full[0][0, 0], 128, bits)
     assert np.array_equal(cu[32:96], cf[32:96])
     # undefined tokens are zero words in the packed form
-    w = codes[0, 0].reshape(2, 4, 16, 4, 2, -1)         # j, g, n, t4, cc, word
+    w = O.lane_words(codes[0, 0], bits).reshape(2, 4, 16, 4, 2, -1)   # j, g, n, t4, cc, word
     live = np.zeros(128, bool)
     live[32:96] = True
     for j in range(2):

@@ -6,13 +6,14 @@ from oracle import ffd_oracle as O
 
 def test_pack_codes_single_token_hand_checked():
     """Token 81 is block 1, t4 = 1, n = 1; dim 16 + 5 is cc = 0, g = 1, e = 5 -> lane 1 + 16 = 17,
-    word 2*1 + 0 = 2, bit 8*(5%4) + 2*(5//4) = 10."""
+    word 2*1 + 0 = 2 (stored at [block, 2 // 4, lane, 2 % 4]), bit 8*(5%4) + 2*(5//4) = 10."""
     codes = np.zeros((128, 128), dtype=np.int64)
     codes[81, 16 + 5] = 3
     p = O.pack_codes(codes)
+    assert p.shape == (2, 2, 64, 4)
     nz = np.argwhere(p)
-    assert nz.tolist() == [[1, 17, 2]]
-    assert int(p[1, 17, 2]) == 3 << 10
+    assert nz.tolist() == [[1, 0, 17, 2]]
+    assert int(p[1, 0, 17, 2]) == 3 << 10
 
 
 def test_pack_codes_fast_equals_loop_and_roundtrips():
