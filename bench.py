@@ -92,7 +92,7 @@ def algorithmic_bytes(case, mask, S, bits=2):
             gather_tokens += int(toks.sum())
     gather = GATHER_BYTES_PER_TOKEN * gather_tokens
     io = case.B * case.Hq * (2 * D + 2 * D + 4)                  # q in, out, lse
-    partials = 2 * case.B * case.Hq * S * (D + 2) * 4              # written, then read by the merge
+    partials = 2 * case.B * case.Hq * (S + 1) * (D + 2) * 4        # (S + 1) rows per head, written, then merged
     return dict(scan=scan, gather=gather, io=io, partials=partials,
                 total=scan + gather + io + partials, gather_tokens=gather_tokens)
 
@@ -206,6 +206,7 @@ class Runner:
         self.q, self.k, self.v = up(case.q), up(case.k), up(case.v)
         self.lens = torch.from_numpy(case.seq_lens.astype(np.int32)).to(dev)
         self.S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, splits)
+        self.Sd = ffd.dense_resolve_splits(case.B, case.Hkv, case.Lcap, splits)   # the dense path's own count
         self.ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev)
         self.dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev, dense=True)
         self.qk = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
@@ -439,7 +440,7 @@ def context_sweep(lengths_k, splits, flush_mib, delta, steps, graph):
         out[f"{lk}K"] = {"ffd_us": round(f_us, 2), "dense_us": round(d_us, 2),
                          "speedup_vs_dense": round(d_us / f_us, 2),
                          "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
-                         "dense_tbps": round(dense_bytes(case, r.S) / (d_us * 1e-6) / 1e12, 3),
+                         "dense_tbps": round(dense_bytes(case, r.Sd) / (d_us * 1e-6) / 1e12, 3),
                          "keep_union_tokens": round(nb["gather_tokens"] / float(case.seq_lens.sum() * case.Hkv), 5)}
         del r
         import torch
@@ -459,7 +460,7 @@ def workload_sweep(splits, flush_mib, steps):
         d_ms, _ = r.time(r.dense_step, steps, 3)
         d_us = float(d_ms.mean() * 1e3)
         entry = {"dense_us": round(d_us, 2),
-                 "dense_tbps": round(dense_bytes(case, r.S) / (d_us * 1e-6) / 1e12, 3)}
+                 "dense_tbps": round(dense_bytes(case, r.Sd) / (d_us * 1e-6) / 1e12, 3)}
         for delta in case.deltas:
             keep = r.mask_for(delta)
             nb = algorithmic_bytes(case, keep, r.S)
@@ -524,7 +525,7 @@ def main():
     # dense flash-decode baseline, same protocol
     dms, _ = r.time(r.graph(r.dense_step) if args.graph else r.dense_step, args.dense_steps, 3)
     dense_us = float(dms.mean() * 1e3)
-    dbytes = dense_bytes(case, S)
+    dbytes = dense_bytes(case, r.Sd)
 
     sweep = {}
     for d in [float(x) for x in args.sweep_deltas.split(",") if x.strip()]:

@@ -204,11 +204,17 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
                                float softmax_scale, void* out, float* lse,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Number of splits a call with this num_splits (0 = automatic) will use. 0 on invalid input. */
+/* Number of splits an ffd_decode_attention call with this num_splits (0 = automatic) will use: the
+ * automatic count gives the refinement (S + 1) * B * Hkv <= 256 workgroups, one per CU of an MI355X.
+ * 0 on invalid input. */
 int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
-/* Workspace bytes needed by ffd_decode_attention for these arguments (enough for the dense entry
- * point too). With S = ffd_resolve_splits(...), P = B * Hkv KV groups, G = Hq / Hkv, C = Lcap / 64
+/* The same for ffd_dense_decode_attention, whose automatic count allows 512 workgroups (B * Hkv * S). */
+int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
+
+/* Workspace bytes needed by ffd_decode_attention for these arguments: the larger of the layout below
+ * and ffd_dense_workspace_bytes(...), so it serves the dense entry point too. With
+ * S = ffd_resolve_splits(...), P = B * Hkv KV groups, G = Hq / Hkv, C = Lcap / 64
  * blocks and S1 scan splits per group (chosen by the library from B, Hkv, Lcap), the regions, each
  * starting on a 256-byte boundary, are: partials (S * P + P) * G * (D + 2) * 4 bytes, table P * 8,
  * kept counts P * S1 * 4, kept lists P * C * 4, block scores P * C * G * 4.
@@ -216,7 +222,7 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
 
 /* Workspace bytes needed by ffd_dense_decode_attention: B * Hq * S * (D + 2) * 4 (fp32 partials
- * m, l, acc) with S = ffd_resolve_splits(...). 0 on invalid input. */
+ * m, l, acc) with S = ffd_dense_resolve_splits(...). 0 on invalid input. */
 size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits);
 
 /* Static, human-readable name of a status code. */

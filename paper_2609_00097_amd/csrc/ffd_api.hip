@@ -1,4 +1,5 @@
 // C ABI of the FFD decode-attention library: argument checks, split choice, kernel launches.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -10,19 +11,23 @@ using namespace ffd;
 
 namespace {
 
-// Automatic split count: the FFD refinement grid has W + B*Hkv = (S + 1) * B*Hkv workgroups of equal
-// work, which should not exceed two per CU on the 256 CUs: a third workgroup on a few CUs makes those
-// CUs finish last (at 4 x 128K, delta 7: 544 workgroups 148 us, 480 workgroups 133 us).
-constexpr int kTargetWorkgroups = 512;
+// Automatic split counts. The FFD refinement grid has W + B*Hkv = (S + 1) * B*Hkv workgroups of
+// equal work; it should not exceed one per CU on the 256 CUs, because a CU serves its older
+// workgroup's memory requests first, so a second workgroup on a CU finishes its share about 3 us
+// later (at 4 x 128K, delta 5: S = 7 (256 workgroups) 60.0 us per step; S = 8 (288) 65.2 us;
+// S = 15 (512) 62.2 us; S = 6 (224) 62.3 us). The dense path keeps two workgroups per CU, its best
+// split count (S = 7 measured 1 % slower at 4 x 128K).
+constexpr int kFfdTargetWorkgroups = 256;
+constexpr int kDenseTargetWorkgroups = 512;
 constexpr int kMinBlocksPerSplit = 8;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
+int resolve_splits(int B, int Hkv, int Lcap, int num_splits, int target = kFfdTargetWorkgroups) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
     if (num_splits > 0) return num_splits;
     const long long pairs = (long long)B * Hkv;
-    long long s = kTargetWorkgroups / pairs - 1;
+    long long s = target / pairs - 1;
     const long long cap = (long long)(Lcap / FFD_BLOCK) / kMinBlocksPerSplit;
     if (s > cap) s = cap;
     if (s < 1) s = 1;
@@ -118,7 +123,7 @@ FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
 int attention_common_checks(const void* q, const void* v, const int32_t* seq_lens, int B, int Hq,
                             int Hkv, int Lcap, int D, int num_splits, float softmax_scale,
                             const void* out, const float* lse, const void* ws, size_t ws_bytes,
-                            int* S_out) {
+                            int target, int* S_out) {
     int st = check_shapes(B, Hq, Hkv, Lcap, D);
     if (st != FFD_OK) return st;
     if (num_splits < 0 || num_splits > FFD_MAX_SPLITS) return FFD_ERR_INVALID_ARGUMENT;
@@ -128,7 +133,7 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
     if (!aligned16(q) || !aligned16(v) || !aligned16(out) || !aligned16(ws)) return FFD_ERR_INVALID_ARGUMENT;
     if ((reinterpret_cast<uintptr_t>(seq_lens) & 3u) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
         return FFD_ERR_INVALID_ARGUMENT;
-    const int S = resolve_splits(B, Hkv, Lcap, num_splits);
+    const int S = resolve_splits(B, Hkv, Lcap, num_splits, target);
     if (S <= 0) return FFD_ERR_INVALID_ARGUMENT;
     *S_out = S;
     return FFD_OK;
@@ -173,19 +178,24 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
     return resolve_splits(B, Hkv, Lcap, num_splits);
 }
 
+int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
+    return resolve_splits(B, Hkv, Lcap, num_splits, kDenseTargetWorkgroups);
+}
+
+size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
+    if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
+    const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits, kDenseTargetWorkgroups);
+    if (S <= 0) return 0;
+    return partials_bytes(B, Hq, S, D);
+}
+
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
     const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
     if (S <= 0) return 0;
     if ((long long)B * Hkv > (1LL << 20) || Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return 0;
-    return ffd_layout(B, Hq, Hkv, Lcap, D, S).total;
-}
-
-size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
-    if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
-    const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
-    if (S <= 0) return 0;
-    return partials_bytes(B, Hq, S, D);
+    // enough for the dense entry point with the same num_splits too
+    return std::max(ffd_layout(B, Hq, Hkv, Lcap, D, S).total, ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits));
 }
 
 const char* ffd_status_string(int status) {
@@ -265,7 +275,7 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     int st = check_bits(thumb_bits);
     if (st != FFD_OK) return st;
     st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
-                                     lse, workspace, workspace_bytes, &S);
+                                     lse, workspace, workspace_bytes, kFfdTargetWorkgroups, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
     if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
@@ -341,7 +351,7 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
                                hipStream_t stream) {
     int S = 0;
     int st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
-                                     lse, workspace, workspace_bytes, &S);
+                                     lse, workspace, workspace_bytes, kDenseTargetWorkgroups, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k || !aligned16(k)) return FFD_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits))

@@ -24,7 +24,7 @@ STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
 
 EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
            "ffd_dense_decode_attention",
-           "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
+           "ffd_resolve_splits", "ffd_dense_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
 
 class FfdLibraryError(RuntimeError):
@@ -68,13 +68,14 @@ def lib() -> ctypes.CDLL:
     so.ffd_decode_attention_ex.argtypes = so.ffd_decode_attention.argtypes + [ctypes.POINTER(DecodeExtras)]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
     so.ffd_resolve_splits.argtypes = [I, I, I, I]
+    so.ffd_dense_resolve_splits.argtypes = [I, I, I, I]
     for name in ("ffd_workspace_bytes", "ffd_dense_workspace_bytes"):
         getattr(so, name).argtypes = [I, I, I, I, I, I]
         getattr(so, name).restype = SZ
     so.ffd_status_string.argtypes = [I]
     so.ffd_status_string.restype = ctypes.c_char_p
     for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
-                 "ffd_dense_decode_attention", "ffd_resolve_splits"):
+                 "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_dense_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
     return so
@@ -105,7 +106,13 @@ def _need(t, name, dtype, shape=None):
 
 
 def resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
+    """Splits an FFD call with this ``num_splits`` uses (0 = automatic)."""
     return lib().ffd_resolve_splits(B, Hkv, Lcap, num_splits)
+
+
+def dense_resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
+    """Splits a dense call with this ``num_splits`` uses (0 = automatic)."""
+    return lib().ffd_dense_resolve_splits(B, Hkv, Lcap, num_splits)
 
 
 def workspace_bytes(B: int, Hq: int, Hkv: int, Lcap: int, num_splits: int = 0,

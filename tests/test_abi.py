@@ -26,7 +26,7 @@ def so():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
-              "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes",
+              "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_dense_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes",
               "ffd_status_string"):
         assert n in names
 
@@ -43,8 +43,12 @@ def test_status_strings(so):
 
 
 def test_splits_and_workspace_sizes(so):
-    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 15           # (15 + 1) * 32 = 512 refinement workgroups
-    assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8
+    assert so.ffd_resolve_splits(4, 8, 131072, 0) == 7            # (7 + 1) * 32 = 256 refinement workgroups
+    assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8              # capped: 64 blocks / 8 per split
+    assert so.ffd_resolve_splits(4, 6, 131072, 0) == 9            # (9 + 1) * 24 = 240 <= 256
+    assert so.ffd_resolve_splits(64, 8, 131072, 0) == 1           # at least one split
+    assert so.ffd_dense_resolve_splits(4, 8, 131072, 0) == 15     # dense: 512 workgroups
+    assert so.ffd_dense_resolve_splits(4, 8, 131072, 5) == 5
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
     # partials (S*P + P)*G*(D+2)*4 | table P*8 | counts P*S1*4 | lists P*C*4 | block scores P*C*G*4,
@@ -52,8 +56,10 @@ def test_splits_and_workspace_sizes(so):
     up = lambda x: -(-x // 256) * 256
     P, G, C = 32, 4, 2048
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
-        up((15 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
+        up((7 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
         + P * C * G * 4)
+    # the dense path's partials (S = 15) are larger than the FFD layout for few blocks
+    assert so.ffd_workspace_bytes(4, 32, 8, 8192, 128, 0) == 4 * 32 * 15 * 130 * 4
     P, G, C = 2, 8, 64
     assert so.ffd_workspace_bytes(1, 16, 2, 4096, 128, 3) == (
         up((3 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 4 * 4) + up(P * C * 4)
