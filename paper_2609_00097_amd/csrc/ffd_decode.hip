@@ -48,7 +48,7 @@ namespace {
 #define FFD_REFINE_RING 2
 #endif
 #ifndef FFD_REFINE_OCC
-#define FFD_REFINE_OCC 3
+#define FFD_REFINE_OCC 2
 #endif
 constexpr int kRing2 = FFD_SCAN_RING;         // 2-bit scan loads in flight per wave (blocks)
 constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
@@ -150,6 +150,52 @@ __device__ __forceinline__ void build_query_consts(QueryLds<NT>& sm, const uint3
         for (int cc = 0; cc < 2; ++cc)
             hc.A[t][cc] = *reinterpret_cast<const v4i*>(&sm.limbs[limb][hrow][64 * cc + 16 * g]);
         const int hh = 4 * t + g;      // this lane's output head
+        hc.live[t] = hh < G;
+        hc.sumq[t] = hc.live[t] ? sm.sumq[hh] : 0;
+        hc.kap[t] = hc.live[t] ? sm.kap[hh] : 0.f;
+        hc.kap2[t] = hc.live[t] ? sm.kap2[hh] : 0.f;
+    }
+}
+
+// The same constants built by one wave alone, with no workgroup barrier: the wave computes every
+// head (qa[h]: this lane's dword of head h, any value for h >= G) and writes the whole limb table;
+// every wave of a workgroup writes identical values, so each may read back what it wrote itself
+// (one wave's LDS operations execute in order) without waiting for the others. Bit for bit the
+// values of build_query_consts.
+template <int NT>
+__device__ __forceinline__ void build_query_consts_wave(QueryLds<NT>& sm, const uint32_t (&qa)[4 * NT], int G,
+                                                        float scale, float lv, int lane, HeadConsts<NT>& hc) {
+    const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+    for (int h = 0; h < 4 * NT; ++h) {
+        const bool live = h < G;
+        const float x0 = live ? bf16_lo(qa[h]) : 0.f, x1 = live ? bf16_hi(qa[h]) : 0.f;
+        const float mx = wave_max_dpp(fmaxf(fabsf(x0), fabsf(x1)));
+        int E = 0;
+        (void)frexpf(mx, &E);                       // mx < 2^E (mx == 0 -> E = 0)
+        const int Q0 = (int)rintf(ldexpf(x0, 22 - E));
+        const int Q1 = (int)rintf(ldexpf(x1, 22 - E));
+#pragma unroll
+        for (int li = 0; li < 3; ++li) {
+            const uint32_t pair = ((uint32_t)limb_of(Q0, li) & 0xffu) | (((uint32_t)limb_of(Q1, li) & 0xffu) << 8);
+            reinterpret_cast<uint16_t*>(&sm.limbs[li][h][0])[lane] = (uint16_t)pair;
+        }
+        reinterpret_cast<uint16_t*>(&sm.limbs[3][h][0])[lane] = 0;
+        const int sum = wave_sum_dpp(Q0 + Q1);
+        if (lane == 0) {
+            sm.sumq[h] = sum;
+            sm.kap[h] = ldexpf(scale / lv, E - 23);
+            sm.kap2[h] = ldexpf(scale / (254.f * lv), E - 22);
+        }
+    }
+    wave_lds_fence();
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int hrow = 4 * t + (n >> 2), limb = n & 3;
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc)
+            hc.A[t][cc] = *reinterpret_cast<const v4i*>(&sm.limbs[limb][hrow][64 * cc + 16 * g]);
+        const int hh = 4 * t + g;
         hc.live[t] = hh < G;
         hc.sumq[t] = hc.live[t] ? sm.sumq[hh] : 0;
         hc.kap[t] = hc.live[t] ? sm.kap[hh] : 0.f;
@@ -577,11 +623,15 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const int G = a.G, S1 = a.S1, npairs = a.npairs;
 
     // ---- allocation: total kept N, then this workgroup's KV group ---------------------------
-    // Usual case: all scan counts fit in LDS. Thread t loads counts [16t, 16t + 16) and one
-    // workgroup scan gives their exclusive prefix in (group, split) order, so N, every group's
-    // n_x and the group's split prefix all come from LDS. Otherwise the counts are summed per
-    // group in passes of kPairChunk groups with LDS atomics.
+    // Usual case (at most 1024 scan counts and 256 KV groups): every wave computes the whole
+    // allocation on its own, with no workgroup barrier. Lane l loads counts [16l, 16l + 16), one
+    // wave prefix gives their exclusive prefix in (group, split) order, which every wave writes to
+    // LDS (identical values, so each reads back its own writes), then lane l allocates groups
+    // 4l .. 4l + 3 and a second wave prefix numbers their workgroups. Larger inputs: all scan counts
+    // kept in LDS with workgroup scans (up to 4096), else summed per group in passes of kPairChunk
+    // groups with LDS atomics.
     const int total = npairs * S1;
+    const bool fast = total <= 16 * 64 && npairs <= 4 * 64;
     const bool cached = total <= kCountCache && npairs <= kPairChunk;
     int N = 0, running = 0, half = 0;
     auto scan = [&](int v, int* tot) {
@@ -590,15 +640,71 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         return e;
     };
     const long long W = a.W;
+    // ceil(n_x * min(W, N) / N) workgroups for n_x > 0; exact in fp64 (the numerator stays below
+    // 2^52, and fl(u / N) cannot round up to an integer when u < 2^52)
     auto alloc = [&](int nx, long long Weff) {
-        return nx > 0 ? (int)(((long long)nx * Weff + N - 1) / N) : 1;
+        return nx > 0 ? (int)floor(((double)nx * (double)Weff + (double)(N - 1)) / (double)N) : 1;
     };
-    if (cached) {
-        const int i0 = 16 * tid;
+    int x = 0, Qx = 0, Wx = 1, nx = 0;
+    if (fast) {
+        const int i0 = 16 * lane;
         int c[16], sum = 0;
 #pragma unroll
         for (int k = 0; k < 16; k += 4) {
             // the counts region is padded to 256 bytes, so the last int4 stays inside it
+            int4 v = make_int4(0, 0, 0, 0);
+            if (i0 + k < total) v = *reinterpret_cast<const int4*>(a.counts + i0 + k);
+            c[k] = v.x; c[k + 1] = v.y; c[k + 2] = v.z; c[k + 3] = v.w;
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            if (i0 + k >= total) c[k] = 0;
+            sum += c[k];
+        }
+        const int incl = wave_inclusive_scan(sum);
+        N = __builtin_amdgcn_readlane(incl, 63);
+        int run = incl - sum;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            if (i0 + k < total) sm.cnt[i0 + k] = run;
+            run += c[k];
+        }
+        if (lane == 0) sm.cnt[total] = N;
+        wave_lds_fence();
+        const long long Weff = min(W, (long long)max(N, 1));
+        int w4[4], n4[4], s4 = 0;                      // lane l: groups 4l .. 4l + 3
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int xi = 4 * lane + k;
+            n4[k] = xi < npairs ? sm.cnt[(xi + 1) * S1] - sm.cnt[xi * S1] : 0;
+            w4[k] = xi < npairs ? alloc(n4[k], Weff) : 0;
+            s4 += w4[k];
+        }
+        const int winc = wave_inclusive_scan(s4);
+        running = __builtin_amdgcn_readlane(winc, 63);
+        int q0 = winc - s4, hit = -1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (hit < 0 && wg >= q0 && wg < q0 + w4[k]) hit = k;
+            if (hit < 0) q0 += w4[k];
+        }
+        const uint64_t hb = __ballot(hit >= 0);
+        if (hb != 0) {                              // uniform; else wg >= running
+            const int src = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(hb));
+            const int kk = __builtin_amdgcn_readlane(hit, src);
+            x = 4 * src + kk;
+            Qx = __builtin_amdgcn_readlane(q0, src);
+            int wsel = w4[0], nsel = n4[0];
+#pragma unroll
+            for (int k = 1; k < 4; ++k) if (kk == k) { wsel = w4[k]; nsel = n4[k]; }
+            Wx = __builtin_amdgcn_readlane(wsel, src);
+            nx = __builtin_amdgcn_readlane(nsel, src);
+        }
+    } else if (cached) {
+        const int i0 = 16 * tid;
+        int c[16], sum = 0;
+#pragma unroll
+        for (int k = 0; k < 16; k += 4) {
             int4 v = make_int4(0, 0, 0, 0);
             if (i0 + k < total) v = *reinterpret_cast<const int4*>(a.counts + i0 + k);
             c[k] = v.x; c[k + 1] = v.y; c[k + 2] = v.z; c[k + 3] = v.w;
@@ -675,8 +781,10 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         }
     }
     if (wg >= running) return;                      // uniform: beyond the last group's workgroups
-    __syncthreads();
-    const int x = sm.sel[0], Qx = sm.sel[1], Wx = sm.sel[2], nx = sm.sel[3];
+    if (!fast) {
+        __syncthreads();
+        x = sm.sel[0]; Qx = sm.sel[1]; Wx = sm.sel[2]; nx = sm.sel[3];
+    }
     const int b = x / a.Hkv, kvh = x % a.Hkv, hq0 = kvh * G;
     const int p = wg - Qx;
     const int r0 = (int)((long long)p * nx / Wx), r1 = (int)((long long)(p + 1) * nx / Wx);
@@ -694,8 +802,19 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * RBITS);
     const uint32_t* list_bh = a.lists + bh * (size_t)nblk_cap;
 
+    // A share of at most kFastShare blocks (with the fast allocation) is staged by every wave on its
+    // own, like the allocation; a longer one in chunks with workgroup barriers.
+    constexpr int kFastShare = 256;
+    const bool fast_share = fast && r1 - r0 <= kFastShare;
     uint32_t qw[NT];
-    load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
+    uint32_t qa[4 * NT];
+    if (fast_share) {
+#pragma unroll
+        for (int h = 0; h < 4 * NT; ++h)
+            qa[h] = reinterpret_cast<const uint32_t*>(a.q + ((size_t)b * a.Hq + hq0 + min(h, G - 1)) * kD)[lane];
+    } else {
+        load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
+    }
     // exclusive prefix of the group's per-split counts: rank r lies in split s with
     // pref(s) <= r < pref(s + 1), at list position s * bps + r - pref(s)
     if (!cached) {
@@ -713,7 +832,15 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     }
     const int* pref = cached ? sm.cnt + x * S1 : sm.pref;
     const int pref0 = cached ? pref[0] : 0;
-    HeadConsts<NT> hc;                              // built once the share's list loads are issued
+    auto list_entry = [&](int r) {                 // the kept block of rank r: j | keep bits << 24
+        int lo = 0, hi = S1;                        // largest split with pref(split) <= r
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (pref[mid] - pref0 <= r) lo = mid; else hi = mid;
+        }
+        return list_bh[lo * bps + (r - (pref[lo] - pref0))];
+    };
+    HeadConsts<NT> hc;
 
     PvAcc<NT> pv;
     pv.zero();
@@ -745,31 +872,18 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         wave_lds_fence();
     };
 
-    bool consts_ready = false;
-    for (int c = r0; c < r1; c += kChunk) {
-        const int m = min(kChunk, r1 - c);
-        for (int i = tid; i < m; i += kThreads) {
-            const int r = c + i;
-            int lo = 0, hi = S1;                    // largest split with pref(split) <= r
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (pref[mid] - pref0 <= r) lo = mid; else hi = mid;
-            }
-            sm.u.list[i] = list_bh[lo * bps + (r - (pref[lo] - pref0))];
-        }
-        if (!consts_ready) {                        // the query loads and the list loads overlap
-            build_query_consts<NT>(sm.qs, qw, G, a.scale, a.top_level, tid, hc);
-            consts_ready = true;
-        }
-        __syncthreads();
+    // the m list entries staged in LDS: gather with kRefineRing tiles in flight. The refill of the
+    // last round re-reads the share's last tile (clamped): it is still cached, and a conditional
+    // refill would cost more registers than it saves. fast_consts: the query constants are built by
+    // this wave while the first tiles are in flight.
+    auto refine_entries = [&](int m, bool fast_consts) {
         auto block_of = [&](int i) { return (int)(sm.u.list[min(i, m - 1)] & 0xffffffu); };
         RefineTile<NT, RBITS> ring[kRefineRing];
 #pragma unroll
         for (int r = 0; r < kRefineRing; ++r)
             ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh, block_of(r), wave,
                                                   lane, last_row);
-        // the refill of the last round re-reads the share's last tile (clamped): it is still
-        // cached, and a conditional refill would cost more registers than it saves
+        if (fast_consts) build_query_consts_wave<NT>(sm.qs, qa, G, a.scale, a.top_level, lane, hc);
         for (int i0 = 0; i0 < m; i0 += kRefineRing) {
 #pragma unroll
             for (int r = 0; r < kRefineRing; ++r) {
@@ -779,7 +893,41 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                                                       block_of(i + kRefineRing), wave, lane, last_row);
             }
         }
-        __syncthreads();                // the list is rewritten by the next chunk / the epilogue
+    };
+
+    if (fast_share) {
+        // every wave loads the whole share's entries (lane i: ranks r0 + i + 64k) and writes them to
+        // LDS: identical values, read back by the same wave
+        const int m = r1 - r0;
+        uint32_t ent[kFastShare / 64];
+#pragma unroll
+        for (int k = 0; k < kFastShare / 64; ++k) {
+            const int i = lane + 64 * k;
+            ent[k] = i < m ? list_entry(r0 + i) : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kFastShare / 64; ++k) {
+            const int i = lane + 64 * k;
+            if (i < m) sm.u.list[i] = ent[k];
+        }
+        wave_lds_fence();
+        if (m > 0) refine_entries(m, true);
+        else build_query_consts_wave<NT>(sm.qs, qa, G, a.scale, a.top_level, lane, hc);
+        __syncthreads();                            // the list area becomes the epilogue's
+    } else {
+        bool consts_ready = false;
+        for (int c = r0; c < r1; c += kChunk) {
+            const int m = min(kChunk, r1 - c);
+            for (int i = tid; i < m; i += kThreads) sm.u.list[i] = list_entry(c + i);
+            if (!consts_ready) {                    // the query loads and the list loads overlap
+                build_query_consts<NT>(sm.qs, qw, G, a.scale, a.top_level, tid, hc);
+                consts_ready = true;
+            }
+            __syncthreads();
+            refine_entries(m, false);
+            __syncthreads();                // the list is rewritten by the next chunk / the epilogue
+        }
+        if (!consts_ready) __syncthreads();
     }
 
     write_partials<NT>(sm.u.epi, pv, m_run, l_part, wave, lane, G, (size_t)wg * G, 1, a.part_m,

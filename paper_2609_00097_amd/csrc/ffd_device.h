@@ -61,6 +61,37 @@ __device__ __forceinline__ int wave_sum_i(int x) {
     return x;
 }
 
+// Wave-wide reductions through DPP within each 16-lane row and four readlanes across the rows
+// (cheaper than a chain of LDS permutes; the same results, max and integer sums being exact).
+__device__ __forceinline__ float wave_max_dpp(float x) {
+    x = fmaxf(x, dpp_f<kDppXor1>(x));
+    x = fmaxf(x, dpp_f<kDppXor2>(x));
+    x = fmaxf(x, dpp_f<kDppRor4>(x));
+    x = fmaxf(x, dpp_f<kDppRor8>(x));
+    const int v = __float_as_int(x);
+    return fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(v, 0)), __int_as_float(__builtin_amdgcn_readlane(v, 16))),
+                 fmaxf(__int_as_float(__builtin_amdgcn_readlane(v, 32)), __int_as_float(__builtin_amdgcn_readlane(v, 48))));
+}
+__device__ __forceinline__ int wave_sum_dpp(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, kDppXor1, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, kDppXor2, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, kDppRor4, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, kDppRor8, 0xf, 0xf, false);
+    return __builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16) +
+           __builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (lane order).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
 // Orders this wave's LDS writes before its later LDS reads (one wave's LDS ops execute in order;
 // this keeps the compiler from moving them across).
 __device__ __forceinline__ void wave_lds_fence() {

@@ -206,3 +206,27 @@ def test_maximum_capacity():
     torch.cuda.synchronize()
     from tests.gpu_util import compare_dense
     compare_dense(c, dense_out, dense_lse)
+
+
+def test_allocation_for_more_than_1024_kv_groups():
+    """More than 1024 (sequence, KV head) groups: the refinement sums the scan counts per group in
+    passes with LDS atomics instead of its per-wave allocation; outputs against the oracle."""
+    lens = [1 + (37 * b) % 64 for b in range(1030)]
+    c = I.small_case(seed=61, B=1030, Hq=1, Hkv=1, seq_lens=lens, Lcap=64, heavy_frac=0.0)
+    print("case 1030 groups of one block", flush=True)
+    up = Uploaded(c)
+    qk = _quant(up)
+    out, lse, mask = _ffd(up, qk, 5.0)
+    compare_ffd(c, 5.0, out, lse, mask)
+
+
+def test_share_longer_than_the_per_wave_staging():
+    """One split: a single refinement workgroup refines all 1094 kept blocks of the group, staged in
+    two chunks with workgroup barriers (shares of up to 256 blocks are staged by each wave alone)."""
+    c = I.small_case(seed=62, B=1, Hq=4, Hkv=1, seq_lens=(70000,), heavy_frac=0.02)
+    print("case one workgroup, 1094 kept blocks", flush=True)
+    up = Uploaded(c)
+    qk = _quant(up)
+    out, lse, mask = _ffd(up, qk, float("inf"), num_splits=1)
+    assert mask.cpu().numpy()[:, :, :1094].all()
+    compare_ffd(c, float("inf"), out, lse, mask)
