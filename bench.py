@@ -136,18 +136,28 @@ def time_steps(fn, steps, warmup, flush, stream, stages=False):
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "ffd_4x128k_hbm_traffic.json")
 
 
+def code_digest(path):
+    """SHA-256 of a C/HIP source with its comments removed and its whitespace collapsed, so that
+    a comment edit does not void a measurement while any change to the code does."""
+    import hashlib
+    import re
+    with open(path, encoding="utf-8") as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()
+
+
 def measured_traffic(kernel, workload, delta):
     """HBM bytes per launch of `kernel` from the committed counter record (FETCH_SIZE and
     WRITE_SIZE, each scaled by the factor a plain copy of known size gives), or None when the
-    record is for another workload or the kernel sources changed since it was taken."""
-    import hashlib
+    record is for another workload or the kernel code changed since it was taken."""
     if workload != 3 or delta != 5.0 or not os.path.exists(TRAFFIC_RECORD):
         return None, "not measured for this workload"
     rec = json.load(open(TRAFFIC_RECORD))
-    for path, digest in rec["source_sha256"].items():
-        with open(os.path.join(ROOT, path), "rb") as f:
-            if hashlib.sha256(f.read()).hexdigest() != digest:
-                return None, f"stale: {path} changed since the counters were taken"
+    for path, digest in rec["code_sha256"].items():
+        if code_digest(os.path.join(ROOT, path)) != digest:
+            return None, f"stale: {path} changed since the counters were taken"
     k = rec["kernels"].get(kernel)
     if k is None:
         return None, "kernel not in the record"

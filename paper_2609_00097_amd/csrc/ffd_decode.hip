@@ -21,19 +21,18 @@
 //
 // Two kernels, so that each stage's HBM stream is balanced over the whole chip:
 //  * ffd_scan_kernel streams the codes and absmaxes of every block once (the dominant, perfectly
-//    regular stream), keeps each block's per-head maximum score in LDS and, once its stream and the
-//    pseudo-max are done, takes the keep decision per (head, block): the kept blocks, with their
-//    per-head keep bits, form its workgroup's kept list (in block order) in the workspace, plus the
-//    list's length.
+//    regular stream; one 8-wave workgroup per CU whose waves take blocks from an LDS counter), keeps
+//    each block's per-head maximum score in LDS and, once its stream and the pseudo-max are done,
+//    takes the keep decision per (head, block): the kept blocks, with their per-head keep bits, form
+//    its workgroup's kept list (in block order) in the workspace, plus the list's length.
 //  * ffd_refine_kernel gives each (sequence, KV head) a number of workgroups proportional to its
 //    kept blocks (every workgroup computes the same allocation from the scan's counts, so no
 //    cross-workgroup synchronisation is needed); each workgroup refines an equal share of its KV
 //    group's kept blocks, wave w taking 16-token tile w of every block, with several tiles' residual
 //    and value loads in flight, recomputes the scan scores s_hat of each tile from its codes (Eq. 4's
 //    reuse term: the same integer MFMA and fp32 operations as the scan, so the same values; storing
-//    them would cost as many bytes, written then read), and writes one partial (m, l, acc) per
-//    head. lse_merge_kernel
-//    combines the partials of each head, located through a small per-group table.
+//    them would cost as many bytes, written then read), and writes one partial (m, l, acc) per head.
+//    lse_merge_kernel combines the partials of each head, located through a small per-group table.
 #include "ffd_device.h"
 #include "ffd_kernels.h"
 
