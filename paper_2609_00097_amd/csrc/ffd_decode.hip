@@ -314,31 +314,55 @@ struct RefineTile {
     uint32_t m;       // absmax bf16 bits in the low half
 };
 
+// An address every lane holds alike, moved to scalar registers: a buffer resource built from it is
+// then one scalar value (the compiler cannot always see that the block number and the wave index
+// are uniform, and otherwise loops over the lanes' distinct resources).
+template <typename T>
+__device__ __forceinline__ void* uniform_ptr(const T* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+}
+
+// All five loads go through buffer resources based at the tile (the block number is wave-uniform):
+// the per-lane offsets are 32-bit and shared, the per-row ones immediates, which saves the 64-bit
+// address arithmetic of every row (about a tenth of the tile's instructions). The value resource
+// ends at the sequence end, so value rows past it read zeros (their probability is zero).
 template <int NT, int RBITS>
 __device__ __forceinline__ RefineTile<NT, RBITS> load_refine_tile(const int8_t* __restrict__ resid_bh,
                                                                   const uint16_t* __restrict__ v_bh,
                                                                   const uint32_t* __restrict__ codes_bh,
                                                                   const uint16_t* __restrict__ absmax_bh,
-                                                                  int j, int T4, int lane, int last_row) {
+                                                                  int j, int T4, int lane, int L) {
     RefineTile<NT, RBITS> r;
     const int tile = 4 * j + T4;
-    const v4i* rp = reinterpret_cast<const v4i*>(resid_bh) + (size_t)tile * 128 + lane;
-    r.r0 = rp[0];
-    r.r1 = rp[64];
-    r.vt = load_vtile(v_bh, 16 * tile, last_row, lane);
+    const uint32_t lo16 = (uint32_t)lane * 16u;
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        uniform_ptr(resid_bh + (size_t)tile * 2048), (short)0, 2048, kRawBufferWord3);
+    r.r0 = (v4i)__builtin_amdgcn_raw_buffer_load_b128(rr, (int)lo16, 0, 0);
+    r.r1 = (v4i)__builtin_amdgcn_raw_buffer_load_b128(rr, (int)(lo16 + 1024u), 0, 0);
+    const int vrows = __builtin_amdgcn_readfirstlane(min(max(L - 16 * tile, 0), 16));
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        uniform_ptr(v_bh + (size_t)tile * (16 * kD)), (short)0, vrows * (2 * kD), kRawBufferWord3);
+#pragma unroll
+    for (int t = 0; t < 16; ++t) r.vt.v[t] = __builtin_amdgcn_raw_buffer_load_b32(rv, lane * 4 + t * (2 * kD), 0, 0);
     // tile T4 is the lane's words T4*b .. T4*b + b - 1 of block j; word w at [w / 4][lane][w % 4]
-    const uint32_t* cb = codes_bh + (size_t)j * (256 * RBITS) + lane * 4;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        uniform_ptr(codes_bh + (size_t)j * (256 * RBITS)), (short)0, 1024 * RBITS, kRawBufferWord3);
     if constexpr (RBITS == 2) {
-        const uint2 w = *reinterpret_cast<const uint2*>(cb + (T4 >> 1) * 256 + 2 * (T4 & 1));
-        r.cw[0] = w.x; r.cw[1] = w.y;
+        const auto w = __builtin_amdgcn_raw_buffer_load_b64(rc, (int)(lo16 + (T4 >> 1) * 1024u + (T4 & 1) * 8u), 0, 0);
+        r.cw[0] = w[0]; r.cw[1] = w[1];
     } else {
 #pragma unroll
         for (int i = 0; i < RBITS / 4; ++i) {
-            const uint4 w = *reinterpret_cast<const uint4*>(cb + (T4 * (RBITS / 4) + i) * 256);
-            r.cw[4 * i] = w.x; r.cw[4 * i + 1] = w.y; r.cw[4 * i + 2] = w.z; r.cw[4 * i + 3] = w.w;
+            const auto w = __builtin_amdgcn_raw_buffer_load_b128(rc, (int)(lo16 + (T4 * (RBITS / 4) + i) * 1024u), 0, 0);
+            r.cw[4 * i] = w[0]; r.cw[4 * i + 1] = w[1]; r.cw[4 * i + 2] = w[2]; r.cw[4 * i + 3] = w[3];
         }
     }
-    r.m = absmax_bh[(size_t)j * 64 + (lane & 15) * 4 + T4];
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        uniform_ptr(absmax_bh + (size_t)j * 64), (short)0, 128, kRawBufferWord3);
+    r.m = __builtin_amdgcn_raw_buffer_load_b16(ra, ((lane & 15) * 4 + T4) * 2, 0, 0);
     return r;
 }
 
@@ -784,6 +808,12 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         __syncthreads();
         x = sm.sel[0]; Qx = sm.sel[1]; Wx = sm.sel[2]; nx = sm.sel[3];
     }
+    // uniform by construction; said explicitly so that the group's base addresses stay in scalar
+    // registers
+    x = __builtin_amdgcn_readfirstlane(x);
+    Qx = __builtin_amdgcn_readfirstlane(Qx);
+    Wx = __builtin_amdgcn_readfirstlane(Wx);
+    nx = __builtin_amdgcn_readfirstlane(nx);
     const int b = x / a.Hkv, kvh = x % a.Hkv, hq0 = kvh * G;
     const int p = wg - Qx;
     const int r0 = (int)((long long)p * nx / Wx), r1 = (int)((long long)(p + 1) * nx / Wx);
@@ -792,7 +822,6 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const int nblk = (L + kBlock - 1) / kBlock;
     const int nblk_cap = a.Lcap / kBlock;
     const int bps = (nblk + S1 - 1) / S1;
-    const int last_row = max(L, 1) - 1;
     if (p == 0 && tid == 0) a.table[x] = make_int2(Qx, Wx);
 
     const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
@@ -881,7 +910,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
 #pragma unroll
         for (int r = 0; r < kRefineRing; ++r)
             ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh, block_of(r), wave,
-                                                  lane, last_row);
+                                                  lane, L);
         if (fast_consts) build_query_consts_wave<NT>(sm.qs, qa, G, a.scale, a.top_level, lane, hc);
         for (int i0 = 0; i0 < m; i0 += kRefineRing) {
 #pragma unroll
@@ -889,7 +918,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
                 const int i = i0 + r;
                 if (i < m) attend(ring[r], (int)(sm.u.list[i] & 0xffffffu), sm.u.list[i] >> 24);
                 ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh,
-                                                      block_of(i + kRefineRing), wave, lane, last_row);
+                                                      block_of(i + kRefineRing), wave, lane, L);
             }
         }
     };
