@@ -64,10 +64,24 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
 
 
 def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round float64 values to bf16 bit patterns (nearest, ties to even), via float32."""
-    u = np.ascontiguousarray(np.asarray(x, dtype=np.float32)).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    """Round float64 values to bf16 bit patterns: one IEEE round to nearest, ties to even.
+
+    bf16 keeps 8 significant bits over float32's exponent range, so the quantum of a value
+    ``m 2^e`` (``0.5 <= |m| < 1``) is ``2^(e - 8)``, and never finer than the subnormal step
+    ``2^-133``. The value is scaled to units of that quantum (exact), rounded with ``rint``
+    (half to even) and scaled back: a bf16 value, or ``2^128`` and beyond, which becomes infinity.
+    NaN maps to the quiet NaN of its sign; signed zeros and infinities are kept. (Rounding to
+    float32 first would round twice: ``1 + 2^-8 + 2^-30`` would become the tie ``1 + 2^-8`` and
+    then ``1`` instead of ``1 + 2^-7``.)
+    """
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)
+    q = np.maximum(e.astype(np.int64) - 8, -133)
+    with np.errstate(over="ignore", invalid="ignore"):
+        y = np.ldexp(np.rint(np.ldexp(x, -q)), q).astype(np.float32)
+    bits = (np.ascontiguousarray(y).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    nan = np.where(np.signbit(x), np.uint16(0xFFC0), np.uint16(0x7FC0))
+    return np.where(np.isnan(x), nan, bits).astype(np.uint16)
 
 
 # ------------------------------------------------------------------------------------------------
@@ -413,7 +427,11 @@ def lse_abs_error(lse, ref):
 
 
 def near_threshold(sigma, m_tilde, delta, band=1e-3):
-    """Blocks whose score lies within ``band`` of the threshold ``m~ - delta`` (reported apart)."""
+    """Blocks whose score lies strictly within ``band`` of the threshold ``m~ - delta`` of Eq. 1:
+    ``|sigma - (m~ - delta)| < band`` with ``sigma`` finite. Their keep decision may differ between
+    two correct implementations that round the scores differently, so parity reports them apart.
+    ``sigma`` is ``[..., nblk]`` and ``m_tilde`` ``[...]``; an empty block (``sigma = -inf``), an
+    empty window (``m~ = -inf``) and ``delta = inf`` give no near block."""
     thr = np.asarray(m_tilde)[..., None] - delta
     with np.errstate(invalid="ignore"):
         return np.isfinite(sigma) & (np.abs(sigma - thr) < band)

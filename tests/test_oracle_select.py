@@ -145,3 +145,61 @@ def test_pseudo_max_windows():
     assert O.pseudo_max_tokens(100, 64, 256).tolist() == list(range(100))
     assert O.pseudo_max_tokens(10, 0, 3).tolist() == [7, 8, 9]
     assert O.pseudo_max_tokens(0, 64, 256).size == 0
+
+
+# ---- near_threshold: the band around Eq. 1's threshold m~ - delta that parity reports apart ----
+
+def test_near_threshold_hand_values():
+    """Threshold m~ - delta = 10 - 5 = 5 with a band of 2^-10 (exact in binary): strictly inside
+    the band on both sides, not at or beyond its edges, never on the wrong side of m~ + delta."""
+    band = 2.0 ** -10
+    m_t = np.array([10.0])
+    sig = np.array([[5.0, 5.0 + band / 2, 5.0 - band / 2, 5.0 + band, 5.0 - band,
+                     5.0 + 2 * band, 15.0, 10.0, 0.0, -np.inf]])
+    got = O.near_threshold(sig, m_t, 5.0, band)
+    assert got.tolist() == [[True, True, True, False, False, False, False, False, False, False]]
+
+
+def test_near_threshold_default_band_is_one_thousandth():
+    m_t = np.array([3.0, -1.5])
+    sig = np.array([[1.0, 1.0009, 0.9991, 1.0011, 0.9989, 3.0],
+                    [-3.5, -3.4995, -3.5005, -3.498, -3.502, -1.5]])
+    got = O.near_threshold(sig, m_t, 2.0)
+    assert got.tolist() == [[True, True, True, False, False, False],
+                            [True, True, True, False, False, False]]
+
+
+def test_near_threshold_infinite_cases():
+    sig = np.array([[-np.inf, 0.0, 1e30, -1e30]])
+    # an empty window: m~ = -inf, so the threshold is -inf and no finite score is near it
+    assert not O.near_threshold(sig, np.array([-np.inf]), 5.0).any()
+    # delta = inf keeps everything: no score is near the threshold
+    assert not O.near_threshold(sig, np.array([2.0]), np.inf).any()
+    # an empty block (sigma = -inf) is never near, even at an infinite threshold
+    assert not O.near_threshold(np.array([[-np.inf]]), np.array([-np.inf]), 0.0).any()
+    # delta = 0: the band sits around m~ itself
+    assert O.near_threshold(np.array([[2.0, 2.0005, 1.0]]), np.array([2.0]), 0.0).tolist() == [[True, True, False]]
+
+
+def test_near_threshold_broadcasts_heads_over_blocks():
+    """[B, H, nblk] scores against [B, H] pseudo-maxima: each head uses its own threshold."""
+    m_t = np.array([[1.0, 4.0], [0.0, -2.0]])
+    sig = np.stack([m_t - 3.0 + 2e-4, m_t - 3.0 + 0.5, m_t], axis=-1)
+    assert O.near_threshold(sig, m_t, 3.0).tolist() == [[[True, False, False]] * 2] * 2
+    # swapping the heads' thresholds moves every band
+    assert not O.near_threshold(sig[:, ::-1, :1], m_t, 3.0).any()
+
+
+def test_near_threshold_agrees_with_a_loop_over_the_definition():
+    rng = np.random.default_rng(3)
+    m_t = rng.normal(size=4)
+    delta = 1.5
+    sig = (m_t[:, None] - delta) + rng.choice([-1, 1], size=(4, 200)) * rng.uniform(0, 3e-3, size=(4, 200))
+    sig[0, :5] = -np.inf
+    got = O.near_threshold(sig, m_t, delta)
+    for h in range(4):
+        for j in range(200):
+            s = sig[h, j]
+            want = bool(np.isfinite(s) and abs(s - (m_t[h] - delta)) < 1e-3)
+            assert got[h, j] == want
+    assert 100 < got.sum() < 700
