@@ -2,24 +2,34 @@
 
 A step is one ffd_decode_attention call (scan + top-delta decision, refinement + online
 softmax . V, split merge: three kernels) over one batch of synthetic inputs already resident in
-HBM. Every timed step is preceded by an untimed 1 GiB read of another buffer (a float32 sum) that
-evicts the 256 MB Infinity Cache and the L2 with clean lines, so the step streams from HBM as it
-would between the layers of a real decode. The dense baseline is timed the same way. The step is
-also captured once in a HIP graph and its replays timed (``graph_us``); on this stack a replay is
-slower than direct launches, so the headline uses direct launches unless ``--graph`` is given.
+HBM. The headline protocol is the paper's layer-averaged setting (Sec. 4.2): the device holds
+``--layers`` N distinct copies of the whole cache (one per layer: quantized keys, values, and the
+bf16 keys the dense baseline reads), and the timed steps run back to back, step i on layer
+i mod N. A step's data was therefore last touched N - 1 steps earlier, after N - 1 other layers'
+caches (each larger than the 256 MB Infinity Cache at 4 x 128K) streamed through, so every step
+reads from HBM. ``value`` is the elapsed time of the K timed steps divided by K (two events around
+the whole run); per-step percentiles come from a second run with an event between steps. The
+dense baseline is timed the same way.
 
-Prints ONE JSON line. ``value`` is the mean microseconds per decode step (lower is better). Effective HBM bandwidth is the
-algorithmic bytes of the step (scan of every valid token's codes and absmax, residual + values of
-the tokens in blocks kept by any head of a KV group, queries, outputs and split partials) divided
-by the step time. ``roofline`` is the dominant kernel's algorithmic bandwidth from per-kernel HIP
-events (recorded by the library between its kernels, in separate eager steps), with its HBM
-traffic from the committed rocprofv3 counter record. ``stream_ceiling`` measures a plain device copy
-under the same flush protocol. ``--context-sweep`` adds the 4K..256K sweep. ``depth_sweep`` times the
-same step with 4- and 8-bit thumbnails (the 4+8 and 8+8 depths of App. C) beside the 2+8 headline.
-``fidelity`` gives Sec. 5.1's recall (cosine with the dense output) and LSE error and Sec. 5.2's
-pseudo-max gap m - m~ for each delta, with the pseudo-max over thumbnail or refined window scores.
-``selection_rule`` times the fixed-budget (top-k) rule with k matched to top-delta's mean keep
-ratio (Table 3's selection-rule overhead comparison), on the same scan and refinement.
+Beside it, ``flush_protocol`` times the same step on one cache after an untimed 1 GiB read of
+another buffer. That does not evict everything: the FFD working set of a step at 4 x 128K
+(~220 MB) fits the Infinity Cache, and blocks kept on every step partly stay there, so the flush
+figure overstates the HBM rate. The step is also captured in a HIP graph (one replay = one step on
+each layer) and its replays timed (``graph_us``).
+
+Prints ONE JSON line. ``value`` is microseconds per decode step (lower is better). Effective HBM
+bandwidth is the algorithmic bytes of the step (scan of every valid token's codes and absmax,
+residual + values of the tokens in blocks kept by any head of a KV group, queries, outputs and
+split partials) divided by the step time. ``roofline`` is the dominant kernel's algorithmic
+bandwidth from per-kernel HIP events (recorded by the library between its kernels, in separate
+rotating steps), with its HBM traffic from the committed rocprofv3 counter record.
+``stream_ceiling`` measures a plain device copy. ``--context-sweep`` adds the 4K..256K sweep.
+``depth_sweep`` times the same step with 4- and 8-bit thumbnails (the 4+8 and 8+8 depths of
+App. C) beside the 2+8 headline. ``fidelity`` gives Sec. 5.1's recall (cosine with the dense
+output) and LSE error and Sec. 5.2's pseudo-max gap m - m~ for each delta, with the pseudo-max
+over thumbnail or refined window scores. ``selection_rule`` times the fixed-budget (top-k) rule
+with k matched to top-delta's mean keep ratio (Table 3's selection-rule overhead comparison), on
+the same scan and refinement.
 """
 from __future__ import annotations
 
@@ -42,6 +52,11 @@ DENSE_BYTES_PER_TOKEN = 256 + 256     # bf16 keys + values
 METRIC = ("µs/decode step + effective HBM TB/s at 128K ctx; speedup vs dense flash-decode")
 
 
+def log(msg):
+    """A progress line on stderr (the JSON result is the only stdout line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -50,7 +65,10 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = 128K x 4 sequences)")
     ap.add_argument("--delta", type=float, default=5.0)
     ap.add_argument("--splits", type=int, default=0)
-    ap.add_argument("--flush-mib", type=int, default=1024)
+    ap.add_argument("--layers", type=int, default=8,
+                    help="distinct copies of the whole cache the timed steps cycle over (>= 4)")
+    ap.add_argument("--flush-mib", type=int, default=1024,
+                    help="the read flush before each step of the flush_protocol figure")
     ap.add_argument("--dense-steps", type=int, default=20)
     ap.add_argument("--sweep-deltas", default="3,7", help="extra deltas timed (10 steps each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -146,8 +164,9 @@ class TimingEvent:
 
 
 def time_steps(fn, steps, warmup, flush, stream, stages=False):
-    """Event-timed steps, each after a cache flush. With ``stages``, ``fn(events)`` also records
-    four per-stage events inside the step (on the same stream); returns their [steps, 3] durations."""
+    """Event-timed steps on one cache, each after a cache flush (the flush protocol). With
+    ``stages``, ``fn(events)`` also records four per-stage events inside the step (on the same
+    stream); returns their [steps, 3] durations."""
     import torch
     for _ in range(warmup):
         flush.flush()
@@ -169,6 +188,55 @@ def time_steps(fn, steps, warmup, flush, stream, stages=False):
         return ms, wall
     st = np.array([[evs[k].elapsed_time(evs[k + 1]) for k in range(3)] for evs in stage_evs])
     return ms, wall, st
+
+
+def time_rotating(fn, layers, steps, warmup, stream):
+    """The layer-averaged protocol: ``steps`` back-to-back calls ``fn(i % layers)``, timed by two
+    events around the whole run (``mean_ms`` = elapsed / steps); then the same run with a
+    timing-only event between consecutive steps for the per-step spread (``per_step_ms``)."""
+    import torch
+    for i in range(warmup):
+        fn(i % layers)
+    t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t0e.record(stream)
+    for i in range(steps):
+        fn(i % layers)
+    t1e.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    mean_ms = t0e.elapsed_time(t1e) / steps
+    evs = [TimingEvent() for _ in range(steps + 1)]
+    for i in range(warmup):
+        fn(i % layers)
+    for i in range(steps):
+        _record(evs[i], stream)
+        fn(i % layers)
+    _record(evs[steps], stream)
+    torch.cuda.synchronize()
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
+    return mean_ms, per, wall
+
+
+def _record(ev, stream):
+    rc = TimingEvent.runtime().hipEventRecord(ev.h, __import__("ctypes").c_void_p(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+
+def time_rotating_stages(fn, layers, steps, warmup):
+    """Per-kernel durations under the layer-averaged protocol: ``fn(layer, events)`` records the
+    library's four stage events inside each step; returns their [steps, 3] durations (ms)."""
+    import torch
+    for i in range(warmup):
+        fn(i % layers, None)
+    evs = [[TimingEvent() for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        fn(i % layers, evs[i])
+    torch.cuda.synchronize()
+    return np.array([[e[k].elapsed_time(e[k + 1]) for k in range(3)] for e in evs])
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "ffd_4x128k_hbm_traffic.json")
@@ -205,15 +273,17 @@ def measured_traffic(kernel, workload, delta):
 
 
 def cpu_baseline(case, delta, budget_s):
-    """The oracle's decode step (given the quantized keys) on host cores, over a bounded sample of
-    (sequence, KV head) pairs, scaled to the whole step."""
+    """The oracle's decode step (given the quantized keys: Alg. 1 from the pseudo-max on) and its
+    exact dense attention, on host cores, over a bounded sample of (sequence, KV head) pairs, each
+    scaled by token count to the whole step. The FFD figure takes about budget_s; the dense figure
+    is timed on the same pairs."""
     from threadpoolctl import threadpool_info
 
     from oracle import ffd_oracle as O
     pairs = [(b, h) for b in range(case.B) for h in range(case.Hkv)]
     alpha = 1.0 / math.sqrt(case.D)
     G = case.G
-    spent, done, tokens = 0.0, 0, 0
+    spent, dense_spent, done, tokens = 0.0, 0.0, 0, 0
     for b, h in pairs:
         L = int(case.seq_lens[b])
         q = O.bf16_to_f64(case.q[b, h * G:(h + 1) * G])
@@ -223,7 +293,10 @@ def cpu_baseline(case, delta, budget_s):
         t0 = time.perf_counter()
         O.decode_group_quantized(q, codes, M, resid, V, L, delta=delta, n_sink=case.n_sink,
                                  n_local=case.n_local, block=64, alpha=alpha)
-        spent += time.perf_counter() - t0
+        t1 = time.perf_counter()
+        O.dense_attention(q, K, V, L, alpha)
+        dense_spent += time.perf_counter() - t1
+        spent += t1 - t0
         done += 1
         tokens += L
         if spent >= budget_s:
@@ -232,60 +305,74 @@ def cpu_baseline(case, delta, budget_s):
     us_step = spent / tokens * total_tokens * 1e6
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": round(us_step, 1), "unit": "us/step", "cores": int(threads), "kind": "oracle",
+            "dense_value": round(dense_spent / tokens * total_tokens * 1e6, 1),
             "sample": f"{done} of {len(pairs)} (sequence, KV head) pairs of the workload, "
-                      f"{tokens} tokens, {spent:.1f} s, scaled by token count to the whole step; "
-                      f"float64 numpy, host affinity {len(os.sched_getaffinity(0))} CPUs"}
+                      f"{tokens} tokens, {spent:.1f} s for the FFD step (scan, pseudo-max, selection, "
+                      f"refinement, softmax.V) and {dense_spent:.1f} s for exact dense attention "
+                      f"(dense_value), each scaled by token count to the whole step; float64 numpy, "
+                      f"host affinity {len(os.sched_getaffinity(0))} CPUs"}
 
 
 class Runner:
-    """Device buffers of one case, its quantized cache, outputs and workspaces, and the timed
-    FFD / dense steps (eager or replayed from a captured HIP graph)."""
+    """Device buffers of one case: ``layers`` distinct copies of its caches (bf16 keys and values
+    and the quantized keys), outputs and workspaces, and the timed FFD / dense steps (eager or
+    replayed from a captured HIP graph), each on a given layer."""
 
-    def __init__(self, case, splits, flush_mib):
+    def __init__(self, case, splits, flush_mib, layers=1):
         import torch
 
         from paper_2609_00097_amd import ffd
         self.torch, self.ffd, self.case, self.splits = torch, ffd, case, splits
         dev = self.dev = torch.device("cuda:0")
         self.stream = torch.cuda.current_stream(dev)
+        self.n_layers = layers
 
         def up(bits):
             return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
-        self.q, self.k, self.v = up(case.q), up(case.k), up(case.v)
+        self.q = up(case.q)
+        k0, v0 = up(case.k), up(case.v)
         self.lens = torch.from_numpy(case.seq_lens.astype(np.int32)).to(dev)
         self.S = ffd.resolve_splits(case.B, case.Hkv, case.Lcap, splits)
         self.Sd = ffd.dense_resolve_splits(case.B, case.Hkv, case.Lcap, splits)   # the dense path's own count
         self.ws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev)
         self.dws = ffd.new_workspace(case.B, case.Hq, case.Hkv, case.Lcap, splits, dev, dense=True)
-        self.qk = ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev)
         # float32: torch.sum keeps the dtype, so the flush is one read-only reduction (an int32
         # buffer would first be cast to an int64 temporary, i.e. a 2 GiB write before every step)
         self.flush_buf = torch.ones((flush_mib << 20) // 4, dtype=torch.float32, device=dev)
         self.out = torch.empty((case.B, case.Hq, case.D), dtype=torch.bfloat16, device=dev)
         self.lse = torch.empty((case.B, case.Hq), dtype=torch.float32, device=dev)
         self.mask = torch.empty((case.B, case.Hq, case.Lcap // 64), dtype=torch.uint8, device=dev)
-        # the cache write (once per prefill; reported, not part of the step)
+        # layer 0 holds the generated cache; the others are copies at their own addresses
+        self.k = [k0] + [k0.clone() for _ in range(layers - 1)]
+        self.v = [v0] + [v0.clone() for _ in range(layers - 1)]
+        self.qk = [ffd.empty_quantized(case.B, case.Hkv, case.Lcap, dev) for _ in range(layers)]
+        # the cache write (once per prefill; reported, not part of the step), timed on layer 0
         qs, qe = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         self.flush()
         qs.record(self.stream)
-        ffd.quantize_keys(self.k, out=self.qk)
+        ffd.quantize_keys(self.k[0], out=self.qk[0])
         qe.record(self.stream)
+        for layer in range(1, layers):
+            ffd.quantize_keys(self.k[layer], out=self.qk[layer])
         torch.cuda.synchronize()
         self.quant_ms = qs.elapsed_time(qe)
 
     def flush(self):
         self.torch.sum(self.flush_buf)
 
-    def ffd_step(self, delta, events=None, mask=None, top_k=0):
+    def ffd_step(self, delta, layer=0, events=None, mask=None, top_k=0, pseudo_max="thumbnail",
+                 m_tilde=None):
         c = self.case
-        self.ffd.decode_attention(self.q, *self.qk, self.v, self.lens, delta=delta, n_sink=c.n_sink,
-                                  n_local=c.n_local, num_splits=self.splits, workspace=self.ws,
-                                  out=self.out, lse=self.lse, mask=mask, stage_events=events,
-                                  top_k=top_k)
+        self.ffd.decode_attention(self.q, *self.qk[layer], self.v[layer], self.lens, delta=delta,
+                                  n_sink=c.n_sink, n_local=c.n_local, num_splits=self.splits,
+                                  workspace=self.ws, out=self.out, lse=self.lse, mask=mask,
+                                  stage_events=events, top_k=top_k, pseudo_max=pseudo_max,
+                                  m_tilde=m_tilde)
 
-    def dense_step(self):
-        self.ffd.dense_decode_attention(self.q, self.k, self.v, self.lens, num_splits=self.splits,
-                                        workspace=self.dws, out=self.out, lse=self.lse)
+    def dense_step(self, layer=0):
+        self.ffd.dense_decode_attention(self.q, self.k[layer], self.v[layer], self.lens,
+                                        num_splits=self.splits, workspace=self.dws, out=self.out,
+                                        lse=self.lse)
 
     def mask_for(self, delta, top_k=0):
         self.ffd_step(delta, mask=self.mask, top_k=top_k)
@@ -309,59 +396,94 @@ class Runner:
         return g.replay
 
     def time(self, fn, steps, warmup, stages=False):
+        """The flush protocol on one cache (layer 0)."""
         return time_steps(fn, steps, warmup, self, self.stream, stages=stages)
+
+    def rotate(self, fn, steps, warmup):
+        """The layer-averaged protocol: fn(layer) back to back over the layers; returns
+        (mean us per step, per-step us array)."""
+        mean_ms, per, _ = time_rotating(fn, self.n_layers, steps, warmup, self.stream)
+        return mean_ms * 1e3, per * 1e3
+
+    def rotate_stages(self, fn, steps, warmup=3):
+        """Per-kernel durations (us) of fn(layer, events) under the layer-averaged protocol."""
+        return time_rotating_stages(fn, self.n_layers, steps, warmup) * 1e3
+
+    def rotate_graph(self, fn, steps, warmup):
+        """One HIP graph holding one step on each layer, replayed; returns mean us per step."""
+        torch = self.torch
+        replay = self.graph(lambda: [fn(layer) for layer in range(self.n_layers)])
+        reps = max(1, -(-steps // self.n_layers))
+        for _ in range(max(1, warmup // self.n_layers)):
+            replay()
+        t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0e.record(self.stream)
+        for _ in range(reps):
+            replay()
+        t1e.record(self.stream)
+        torch.cuda.synchronize()
+        return t0e.elapsed_time(t1e) * 1e3 / (reps * self.n_layers)
 
 
 def decode_loop(r, delta, steps, warmup):
-    """Decode-loop step: append one token per sequence (ffd_append_kv) then attend. The lengths
-    start 256 tokens below capacity so every timed step has room; each step grows the cache by one
-    token. Times the append alone, append + attention with direct launches, and the same two calls
-    captured once in a HIP graph and replayed (no re-capture as the cache grows)."""
+    """Decode-loop step: append one token per sequence (ffd_append_kv) then attend, on each layer
+    in turn (each layer has its own lengths, advanced by its appends). The lengths start 256 tokens
+    below capacity so every timed step has room. Times the append alone, append + attention with
+    direct launches, and the same calls captured once in a HIP graph (one append + attention per
+    layer) and replayed (no re-capture as the caches grow)."""
     torch, ffd, c = r.torch, r.ffd, r.case
-    room = warmup + steps + 4
     lens0 = torch.clamp(r.lens - 256, min=0)
-    lens = lens0.clone()
+    lens = [lens0.clone() for _ in range(r.n_layers)]
     gen = torch.Generator(device=r.dev).manual_seed(1)
     k_new = torch.randn((c.B, c.Hkv, c.D), device=r.dev, generator=gen).to(torch.bfloat16)
     v_new = torch.randn((c.B, c.Hkv, c.D), device=r.dev, generator=gen).to(torch.bfloat16)
 
-    def append():
-        ffd.append_kv(k_new, v_new, r.qk, lens, k_cache=r.k, v_cache=r.v)
+    def append(layer):
+        ffd.append_kv(k_new, v_new, r.qk[layer], lens[layer], k_cache=r.k[layer], v_cache=r.v[layer])
 
-    def step():
-        append()
-        ffd.decode_attention(r.q, *r.qk, r.v, lens, delta=delta, n_sink=c.n_sink, n_local=c.n_local,
-                             num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse)
-    assert 3 * room <= 256, "not enough room for the appends"
-    lens.copy_(lens0)
-    a_ms, _ = r.time(append, steps, warmup)
-    lens.copy_(lens0)
-    s_ms, _ = r.time(step, steps, warmup)
-    lens.copy_(lens0)
-    g_ms, _ = r.time(r.graph(step), steps, warmup)
-    return {"append_us": round(float(a_ms.mean() * 1e3), 2),
-            "append_plus_attention_us": round(float(s_ms.mean() * 1e3), 2),
-            "graph_append_plus_attention_us": round(float(g_ms.mean() * 1e3), 2),
+    def step(layer):
+        append(layer)
+        ffd.decode_attention(r.q, *r.qk[layer], r.v[layer], lens[layer], delta=delta, n_sink=c.n_sink,
+                             n_local=c.n_local, num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse)
+
+    def reset():
+        for t in lens:
+            t.copy_(lens0)
+    # appends per layer in one measurement: two rotating runs, or the graph's warm-up and replays
+    per_layer = 2 * -(-(warmup + steps) // r.n_layers) + 2
+    assert per_layer <= 256, "not enough room for the appends"
+    reset()
+    a_us, _ = r.rotate(append, steps, warmup)
+    reset()
+    s_us, _ = r.rotate(step, steps, warmup)
+    reset()
+    g_us = r.rotate_graph(step, steps, warmup)
+    return {"append_us": round(float(a_us), 2),
+            "append_plus_attention_us": round(float(s_us), 2),
+            "graph_append_plus_attention_us": round(float(g_us), 2),
             "what": "one token appended per sequence (bf16 K/V rows + quantized key, length advanced "
-                    "on the device) then the decode attention, starting 256 tokens below capacity; "
-                    "the graph is captured once and replayed while the cache grows"}
+                    "on the device) then the decode attention, layer after layer, starting 256 tokens "
+                    "below capacity; the graph (one append + attention per layer) is captured once and "
+                    "replayed while the caches grow"}
 
 
 def depth_sweep(r, delta, depths, steps, dense_us):
-    """The step with b-bit thumbnails (App. C's 4+8 and 8+8): the cache quantized at that depth,
-    the step timed as the headline, and the three kernels timed by library events."""
+    """The step with b-bit thumbnails (App. C's 4+8 and 8+8): every layer's cache quantized at that
+    depth, the step timed as the headline, and the three kernels timed by library events."""
     torch, ffd, c = r.torch, r.ffd, r.case
     saved = r.qk
     out = {}
     for bits in depths:
-        r.qk = ffd.empty_quantized(c.B, c.Hkv, c.Lcap, r.dev, bits)
-        ffd.quantize_keys(r.k, out=r.qk)
+        r.qk = None
+        torch.cuda.empty_cache()
+        r.qk = [ffd.empty_quantized(c.B, c.Hkv, c.Lcap, r.dev, bits) for _ in range(r.n_layers)]
+        for layer in range(r.n_layers):
+            ffd.quantize_keys(r.k[layer], out=r.qk[layer])
         keep = r.mask_for(delta)
         nb = algorithmic_bytes(c, keep, r.S, bits)
-        ms, _ = r.time(lambda: r.ffd_step(delta), steps, 5)
-        _, _, st = r.time(lambda ev: r.ffd_step(delta, events=ev), steps, 3, stages=True)
-        su = st.mean(axis=0) * 1e3
-        us = float(ms.mean() * 1e3)
+        us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
+        su = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev), steps).mean(axis=0)
         scan_bytes = nb["scan"] + c.B * c.Hq * 2 * c.D
         out[f"{bits}+8"] = {"us": round(us, 2), "scan_us": round(float(su[0]), 2),
                             "refine_us": round(float(su[1]), 2), "merge_us": round(float(su[2]), 2),
@@ -369,13 +491,13 @@ def depth_sweep(r, delta, depths, steps, dense_us):
                             "scan_gbps": round(scan_bytes / (float(su[0]) * 1e-6) / 1e9, 1),
                             "keep_head_blocks": round(float(keep.mean()), 5),
                             "speedup_vs_dense": round(dense_us / us, 2)}
-        r.qk = None
-        torch.cuda.empty_cache()
+    r.qk = None
+    torch.cuda.empty_cache()
     r.qk = saved
     return out
 
 
-def selection_rule(r, delta, keep, steps, dense_us, stage_us):
+def selection_rule(r, delta, keep, steps, dense_us, stage_us, td_us):
     """Table 3's comparison on one scan and refinement: the fixed-budget rule with k = top-delta's
     mean kept blocks per head, timed like the headline, with its own kernels' event times."""
     c = r.case
@@ -384,12 +506,10 @@ def selection_rule(r, delta, keep, steps, dense_us, stage_us):
     k = max(1, int(round(kept / float(c.B * c.Hq))))
     kk = r.mask_for(delta, top_k=k)
     bk = algorithmic_bytes(c, kk, r.S)
-    ms, _ = r.time(lambda: r.ffd_step(delta, top_k=k), steps, 5)
-    _, _, st = r.time(lambda ev: r.ffd_step(delta, events=ev, top_k=k), steps, 3, stages=True)
-    su = st.mean(axis=0) * 1e3
-    us = float(ms.mean() * 1e3)
+    us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer, top_k=k), steps, 5)
+    su = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev, top_k=k), steps).mean(axis=0)
     ratio = lambda m: float(np.mean(np.concatenate([m[b, :, :nb[b]].ravel() for b in range(c.B)])))
-    return {"k": k, "top_k_us": round(us, 2),
+    return {"k": k, "top_k_us": round(us, 2), "top_delta_us": round(td_us, 2),
             "top_k_keep_head_blocks": round(ratio(kk), 5),
             "top_delta_keep_head_blocks": round(ratio(keep), 5),
             "top_k_keep_union_tokens": round(bk["gather_tokens"] / float(c.seq_lens.sum() * c.Hkv), 5),
@@ -401,7 +521,7 @@ def selection_rule(r, delta, keep, steps, dense_us, stage_us):
             "what": "top-k keeps per head the k blocks with the largest thumbnail block scores (scan, "
                     "then a per-(sequence, KV head) radix-select kernel, then the refinement recomputing "
                     "the kept blocks' thumbnail scores); k = top-delta's mean kept blocks per head at "
-                    "this delta; stage times from library events in separate steps"}
+                    "this delta; layer-averaged protocol; stage times from library events in separate steps"}
 
 
 def exact_max(r):
@@ -415,7 +535,7 @@ def exact_max(r):
         if L == 0:
             m[b] = float("-inf")
             continue
-        kf = r.k[b, :, :L].float()                                         # [Hkv, L, D]
+        kf = r.k[0][b, :, :L].float()                                      # [Hkv, L, D]
         qf = r.q[b].float().view(c.Hkv, c.G, c.D).transpose(1, 2).contiguous()   # [Hkv, D, G]
         m[b] = (torch.matmul(kf, qf).amax(dim=1) * alpha).reshape(c.Hq)
         del kf
@@ -425,7 +545,7 @@ def exact_max(r):
 def fidelity(r, deltas, steps):
     """Sec. 5.1 recall (cosine of the FFD and dense outputs per head) and LSE error, Sec. 5.2 gap
     m - m~ per head, keep ratio, and the step time, for each delta and pseudo-max source."""
-    torch, ffd, c = r.torch, r.ffd, r.case
+    torch, c = r.torch, r.case
     r.dense_step()
     d_out, d_lse = r.out.float().cpu().numpy(), r.lse.cpu().numpy()
     m = exact_max(r).cpu().numpy()
@@ -433,32 +553,30 @@ def fidelity(r, deltas, steps):
     res = {}
     for pm in ("thumbnail", "refined"):
         for d in deltas:
-            ffd.decode_attention(r.q, *r.qk, r.v, r.lens, delta=d, n_sink=c.n_sink, n_local=c.n_local,
-                                 num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse, mask=r.mask,
-                                 m_tilde=mt, pseudo_max=pm)
+            r.ffd_step(d, mask=r.mask, pseudo_max=pm, m_tilde=mt)
             torch.cuda.synchronize()
             o, l = r.out.float().cpu().numpy(), r.lse.cpu().numpy()
             keep = r.mask.cpu().numpy().astype(bool)
             cos = np.sum(o * d_out, -1) / (np.linalg.norm(o, axis=-1) * np.linalg.norm(d_out, axis=-1))
             err = np.abs(l - d_lse)
             gap = m - mt.cpu().numpy()
-            ms, _ = r.time(lambda: ffd.decode_attention(
-                r.q, *r.qk, r.v, r.lens, delta=d, n_sink=c.n_sink, n_local=c.n_local,
-                num_splits=r.splits, workspace=r.ws, out=r.out, lse=r.lse, pseudo_max=pm), steps, 3)
+            us, _ = r.rotate(lambda layer: r.ffd_step(d, layer, pseudo_max=pm), steps, 3)
             res[f"{pm}/delta={d:g}"] = {
-                "us": round(float(ms.mean() * 1e3), 2),
+                "us": round(float(us), 2),
                 "keep_head_blocks": round(float(keep.mean()), 5),
                 "recall_min": round(float(cos.min()), 6), "recall_mean": round(float(cos.mean()), 6),
                 "lse_err_max": round(float(err.max()), 5), "lse_err_mean": round(float(err.mean()), 5),
                 "gap_p50_p90_max": [round(float(np.percentile(gap, p)), 4) for p in (50, 90, 100)],
                 "gap_zero_frac": round(float(np.mean(gap <= 0)), 4)}
     return {"what": "FFD vs the dense kernel's output (cosine per head, |lse - lse_dense|), "
-                    "m - m~ with m the exact max over all tokens (float32 on the GPU); 128 heads",
+                    "m - m~ with m the exact max over all tokens (float32 on the GPU); 128 heads; "
+                    "step time under the layer-averaged protocol",
             **res}
 
 
 def stream_ceiling(r, reps=10):
-    """Plain read (float32 sum) and plain copy of 512 MiB under the bench's flush protocol."""
+    """Plain copy of 512 MiB (read + write bytes), median of ``reps`` event-timed copies, each
+    after the 1 GiB read flush."""
     torch = r.torch
     n = (512 << 20) // 4
     src = torch.ones(n, dtype=torch.float32, device=r.dev)
@@ -471,20 +589,17 @@ def stream_ceiling(r, reps=10):
                                          "10, HIP events; counts read + write bytes"}
 
 
-def context_sweep(lengths_k, splits, flush_mib, delta, steps, graph):
-    """FFD and dense step times at workload 2's layout for each context length."""
+def context_sweep(lengths_k, splits, flush_mib, delta, steps, layers):
+    """FFD and dense step times at workload 2's layout for each context length (layer-averaged)."""
     import ffd_inputs as I
     out = {}
     for lk in lengths_k:
         case = I.context_case(lk * 1024)
-        r = Runner(case, splits, flush_mib)
+        r = Runner(case, splits, flush_mib, layers)
         keep = r.mask_for(delta)
         nb = algorithmic_bytes(case, keep, r.S)
-        ffd_fn = r.graph(lambda: r.ffd_step(delta)) if graph else (lambda: r.ffd_step(delta))
-        dense_fn = r.graph(r.dense_step) if graph else r.dense_step
-        f_ms, _ = r.time(ffd_fn, steps, 5)
-        d_ms, _ = r.time(dense_fn, steps, 5)
-        f_us, d_us = float(f_ms.mean() * 1e3), float(d_ms.mean() * 1e3)
+        f_us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
+        d_us, _ = r.rotate(r.dense_step, steps, 5)
         out[f"{lk}K"] = {"ffd_us": round(f_us, 2), "dense_us": round(d_us, 2),
                          "speedup_vs_dense": round(d_us / f_us, 2),
                          "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
@@ -496,24 +611,23 @@ def context_sweep(lengths_k, splits, flush_mib, delta, steps, graph):
     return out
 
 
-def workload_sweep(splits, flush_mib, steps):
-    """FFD and dense step times for workloads 1..5 (each at its deltas), keep ratios, algorithmic TB/s."""
+def workload_sweep(splits, flush_mib, steps, layers):
+    """FFD and dense step times for workloads 1..5 (each at its deltas), keep ratios, algorithmic
+    TB/s, layer-averaged."""
     import torch
 
     import ffd_inputs as I
     out = {}
     for wl in range(1, 6):
         case = I.workload(wl)
-        r = Runner(case, splits, flush_mib)
-        d_ms, _ = r.time(r.dense_step, steps, 3)
-        d_us = float(d_ms.mean() * 1e3)
+        r = Runner(case, splits, flush_mib, layers)
+        d_us, _ = r.rotate(r.dense_step, steps, 3)
         entry = {"dense_us": round(d_us, 2),
                  "dense_tbps": round(dense_bytes(case, r.Sd) / (d_us * 1e-6) / 1e12, 3)}
         for delta in case.deltas:
             keep = r.mask_for(delta)
             nb = algorithmic_bytes(case, keep, r.S)
-            f_ms, _ = r.time(lambda: r.ffd_step(delta), steps, 5)
-            f_us = float(f_ms.mean() * 1e3)
+            f_us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
             valid = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel() for b in range(case.B)])
             entry[f"delta={delta:g}"] = {
                 "ffd_us": round(f_us, 2), "speedup_vs_dense": round(d_us / f_us, 2),
@@ -532,20 +646,30 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(each (sequence, KV head) pair is independent; see the design notes)", file=sys.stderr)
         sys.exit(2)
+    if args.layers < 1:
+        print("--layers must be at least 1", file=sys.stderr)
+        sys.exit(2)
 
     import torch  # noqa: F401  (initialises the HIP runtime before the library is used)
 
     import ffd_inputs as I
 
+    log(f"generating workload {args.workload}")
     case = I.workload(args.workload)
-    r = Runner(case, args.splits, args.flush_mib)
+    log(f"uploading {args.layers} cache copies and quantizing")
+    r = Runner(case, args.splits, args.flush_mib, args.layers)
     S = r.S
+    delta = args.delta
 
     # the measured mask gives the algorithmic bytes (mask output off in the timed steps)
-    keep = r.mask_for(args.delta)
+    keep = r.mask_for(delta)
     nbytes = algorithmic_bytes(case, keep, S)
 
-    eager_ms, wall = r.time(lambda: r.ffd_step(args.delta), args.steps, args.warmup)
+    ffd_fn = lambda layer: r.ffd_step(delta, layer)        # noqa: E731
+    log("timing the FFD step (layer-averaged)")
+    t0 = time.perf_counter()
+    eager_us, per_step = r.rotate(ffd_fn, args.steps, args.warmup)
+    wall = time.perf_counter() - t0
     if args.profile_only:
         if args.copy_mib > 0:
             src = torch.ones((args.copy_mib << 20) // 4, dtype=torch.int32, device=r.dev)
@@ -554,45 +678,54 @@ def main():
             torch.cuda.synchronize()
             dst.copy_(src)
             torch.cuda.synchronize()
-        print(json.dumps({"profile_only": True, "ffd_us_mean": float(eager_ms.mean() * 1e3),
+        print(json.dumps({"profile_only": True, "ffd_us_mean": eager_us, "layers": args.layers,
                           "copy_mib": args.copy_mib}))
         return
-    graph_ms, graph_wall = r.time(r.graph(lambda: r.ffd_step(args.delta)), args.steps, args.warmup)
-    ms = graph_ms if args.graph else eager_ms
-    wall = graph_wall if args.graph else wall
-    us = float(ms.mean() * 1e3)
-    eager_us = float(eager_ms.mean() * 1e3)
-    graph_us = float(graph_ms.mean() * 1e3)
+    log(f"FFD step {eager_us:.2f} us; graph replay, flush protocol, stages, dense")
+    graph_us = r.rotate_graph(ffd_fn, args.steps, args.warmup)
+    us = graph_us if args.graph else eager_us
     tbps = nbytes["total"] / (us * 1e-6) / 1e12
 
-    # per-kernel durations from library-recorded events, in separate eager steps: the event
+    # the flush protocol on one cache, for comparison with the layer-averaged figure
+    flush_ms, _ = r.time(lambda: r.ffd_step(delta), max(20, args.steps // 2), 5)
+    flush_us = float(flush_ms.mean() * 1e3)
+    _, _, flush_stage_ms = r.time(lambda ev: r.ffd_step(delta, events=ev), 20, 3, stages=True)
+    flush_stage_us = flush_stage_ms.mean(axis=0) * 1e3
+
+    # per-kernel durations from library-recorded events, in separate rotating steps: the event
     # markers between kernels add a few microseconds of gap, so these steps are not the headline
-    _, _, stage_ms = r.time(lambda ev: r.ffd_step(args.delta, events=ev), max(10, args.steps // 2), 3,
-                            stages=True)
+    stage_us = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev),
+                               max(16, args.steps // 2)).mean(axis=0)
 
     # dense flash-decode baseline, same protocol
-    dms, _ = r.time(r.graph(r.dense_step) if args.graph else r.dense_step, args.dense_steps, 3)
-    dense_us = float(dms.mean() * 1e3)
+    dense_us, _ = r.rotate(r.dense_step, args.dense_steps, 4)
+    if args.graph:
+        dense_us = r.rotate_graph(r.dense_step, args.dense_steps, 4)
     dbytes = dense_bytes(case, r.Sd)
+    dflush_ms, _ = r.time(r.dense_step, 10, 2)
+    dense_flush_us = float(dflush_ms.mean() * 1e3)
 
+    log(f"dense {dense_us:.2f} us; delta sweep")
     sweep = {}
     for d in [float(x) for x in args.sweep_deltas.split(",") if x.strip()]:
         kd = r.mask_for(d)
         bd = algorithmic_bytes(case, kd, S)
-        fn = r.graph(lambda: r.ffd_step(d)) if args.graph else (lambda: r.ffd_step(d))
-        sms, _ = r.time(fn, 20, 3)
-        su = float(sms.mean() * 1e3)
+        su, _ = r.rotate(lambda layer: r.ffd_step(d, layer), 24, 4)
+        ss = r.rotate_stages(lambda layer, ev: r.ffd_step(d, layer, events=ev), 16).mean(axis=0)
         sweep[str(d)] = {"us": round(su, 2), "tbps": round(bd["total"] / (su * 1e-6) / 1e12, 3),
                          "keep_head_blocks": round(float(kd.mean()), 5),
+                         "keep_union_tokens": round(bd["gather_tokens"] / float(np.sum(case.seq_lens) * case.Hkv), 5),
+                         "stages_us": [round(float(x), 2) for x in ss],
+                         "refine_gbps": round(bd["gather"] / (float(ss[1]) * 1e-6) / 1e9, 1),
                          "speedup_vs_dense": round(dense_us / su, 2)}
 
-    stage_us = stage_ms.mean(axis=0) * 1e3
-    selection = selection_rule(r, args.delta, keep, 30, dense_us, stage_us)
+    log("selection rule, copy ceiling, depth sweep, fidelity, decode loop")
+    selection = selection_rule(r, delta, keep, 32, dense_us, stage_us, eager_us)
     ceiling = stream_ceiling(r)
-    depths = depth_sweep(r, args.delta, [int(x) for x in args.depths.split(",") if x.strip()],
-                         20, dense_us)
-    fid = None if args.no_fidelity else fidelity(r, [3.0, 5.0, 7.0], 20)
-    loop = decode_loop(r, args.delta, min(args.steps, 60), 10)      # writes the caches: run last
+    depths = depth_sweep(r, delta, [int(x) for x in args.depths.split(",") if x.strip()],
+                         24, dense_us)
+    fid = None if args.no_fidelity else fidelity(r, [3.0, 5.0, 7.0], 24)
+    loop = decode_loop(r, delta, min(args.steps, 48), 8)      # writes the caches: run last
 
     # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
     stage_bytes = {"ffd_scan_kernel": nbytes["scan"] + case.B * case.Hq * 2 * case.D,
@@ -602,7 +735,7 @@ def main():
     dom = names[int(np.argmax(stage_us))]
     dom_us = float(stage_us[names.index(dom)])
     dom_gbps = stage_bytes[dom] / (dom_us * 1e-6) / 1e9
-    traffic, traffic_src = measured_traffic(dom, args.workload, args.delta)
+    traffic, traffic_src = measured_traffic(dom, args.workload, delta)
 
     valid_blocks = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel()
                                    for b in range(case.B)])
@@ -622,14 +755,16 @@ def main():
         "data": "synthetic",
         "config": {"workload": case.name, "batch": case.B, "context": int(case.Lcap),
                    "q_heads": case.Hq, "kv_heads": case.Hkv, "head_dim": case.D, "kv_block": 64,
-                   "delta": args.delta, "n_sink": case.n_sink, "n_local": case.n_local,
+                   "delta": delta, "n_sink": case.n_sink, "n_local": case.n_local,
                    "num_splits": S, "io": "q/v/out bf16, k as 2-bit codes + int8 residual",
                    "launch": "hip graph replay" if args.graph else "direct (stream-ordered) launches",
-                   "cache_flush_between_steps_mib": args.flush_mib, "cache_flush": "read"},
+                   "protocol": f"layer-averaged: {args.layers} distinct caches, steps back to back, "
+                               f"step i on cache i mod {args.layers}",
+                   "layers": args.layers},
         "effective_tbps": round(tbps, 3),
         "hbm_peak_frac": round(tbps * 1e3 / HBM_PEAK_GBPS, 4),
         "bytes_per_step": nbytes,
-        "us_p10_p50_p90": [round(float(np.percentile(ms, p)) * 1e3, 2) for p in (10, 50, 90)],
+        "us_p10_p50_p90": [round(float(np.percentile(per_step, p)), 2) for p in (10, 50, 90)],
         "eager_us": round(eager_us, 2),
         "graph_us": round(graph_us, 2),
         "keep_head_blocks": round(float(valid_blocks.mean()), 5),
@@ -637,6 +772,13 @@ def main():
         "dense_us": round(dense_us, 2),
         "dense_tbps": round(dbytes / (dense_us * 1e-6) / 1e12, 3),
         "speedup_vs_dense": round(dense_us / us, 2),
+        "flush_protocol": {
+            "what": f"one cache, an untimed {args.flush_mib} MiB read before every step (event-timed "
+                    "per step); part of the kept blocks stay in the Infinity Cache across steps",
+            "ffd_us": round(flush_us, 2), "dense_us": round(dense_flush_us, 2),
+            "effective_tbps": round(nbytes["total"] / (flush_us * 1e-6) / 1e12, 3),
+            "stages_us": {k: round(float(u), 2) for k, u in zip(("scan", "refine", "merge"), flush_stage_us)},
+            "speedup_vs_dense": round(dense_flush_us / flush_us, 2)},
         "delta_sweep": sweep,
         "depth_sweep": {"2+8": {"us": round(eager_us, 2), "scan_us": round(float(stage_us[0]), 2),
                                 "refine_us": round(float(stage_us[1]), 2),
@@ -656,21 +798,22 @@ def main():
                      "kernel": dom, "kernel_us": round(dom_us, 2),
                      "algorithmic_bytes": int(stage_bytes[dom]),
                      "timing": "HIP events (hipEventDisableSystemFence) recorded by the library "
-                               "on the launch stream around each kernel, mean over separate eager "
-                               "steps"},
+                               "on the launch stream around each kernel, mean over separate "
+                               "layer-averaged steps"},
     }
-    if args.context_sweep:
+    if args.context_sweep or args.workload_sweep:
         del r
         torch.cuda.empty_cache()
+    if args.context_sweep:
+        log("context sweep")
         line["context_sweep"] = context_sweep([int(x) for x in args.context_sweep.split(",") if x.strip()],
-                                              args.splits, args.flush_mib, args.delta, 30, args.graph)
+                                              args.splits, args.flush_mib, delta, 32, args.layers)
     if args.workload_sweep:
-        if "r" in locals():
-            del r
-        torch.cuda.empty_cache()
-        line["workload_sweep"] = workload_sweep(args.splits, args.flush_mib, 30)
+        log("workload sweep")
+        line["workload_sweep"] = workload_sweep(args.splits, args.flush_mib, 32, min(args.layers, 4))
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(case, args.delta, args.cpu_seconds)
+        log("CPU oracle baseline")
+        line["cpu_baseline"] = cpu_baseline(case, delta, args.cpu_seconds)
     print(json.dumps(line))
 
 

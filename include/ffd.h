@@ -9,9 +9,11 @@
  *   ffd_append_kv               append one decode token per sequence to the bf16 and quantized
  *                               caches at its device-side length, and advance the length.
  *   ffd_decode_attention        pseudo-max over sink and local tokens (Alg. 1; Eq. 3), b-bit scan and
- *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement that reuses
- *                               the scan dot products (Eq. 4), online-softmax attention over the kept
- *                               blocks, split into partial states merged by log-sum-exp
+ *                               per-block top-delta selection (Alg. 1; Eq. 1), refinement of the kept
+ *                               blocks' logits as the scan score plus the residual term (Eq. 4; the
+ *                               scan score of a kept token is recomputed from its codes, bit for bit
+ *                               the scan's value, rather than stored), online-softmax attention over
+ *                               the kept blocks, split into partial states merged by log-sum-exp
  *                               (flash-decoding, Sec. 2 and Sec. 3.3). Three kernels in order on
  *                               `stream`: scan + selection, refinement + attention, merge.
  *   ffd_dense_decode_attention  exact dense decode attention over the bf16 cache (the dense
@@ -20,7 +22,8 @@
  * Conventions for every entry point
  *  - Tensor arguments are DEVICE pointers to contiguous row-major buffers owned by the caller.
  *    The library never allocates, frees or retains them, never synchronises the host, and keeps no
- *    mutable global state. Calls are asynchronous on `stream`; outputs are valid once it completes.
+ *    mutable global state apart from each device's compute-unit count, queried once and cached.
+ *    Calls are asynchronous on `stream`; outputs are valid once it completes.
  *  - bf16 tensors are passed as `const void*` holding IEEE bfloat16 bit patterns.
  *  - Shapes: B sequences, Hq query heads, Hkv KV heads (Hq % Hkv == 0, G = Hq / Hkv in {1,2,4,8};
  *    query head h reads KV head h / G), head dimension D == 128, cache capacity Lcap tokens
@@ -205,11 +208,14 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Number of splits an ffd_decode_attention call with this num_splits (0 = automatic) will use: the
- * automatic count gives the refinement (S + 1) * B * Hkv <= 256 workgroups, one per CU of an MI355X.
+ * automatic count gives the refinement (S + 1) * B * Hkv workgroups, at most one per compute unit of
+ * the current device (its CU count is queried once per device and cached; 256, an MI355X's, if the
+ * query fails). The workspace size depends on it, so size and call on the same device.
  * 0 on invalid input. */
 int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
-/* The same for ffd_dense_decode_attention, whose automatic count allows 512 workgroups (B * Hkv * S). */
+/* The same for ffd_dense_decode_attention, whose automatic count allows two workgroups per compute
+ * unit (B * Hkv * S). */
 int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
 /* Workspace bytes needed by ffd_decode_attention for these arguments: the larger of the layout below

@@ -88,6 +88,9 @@ def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
 # Q1/Q2. Key decomposition k -> {k^quant, k^res} (Sec. 3.1; App. A formulation).
 # ------------------------------------------------------------------------------------------------
 
+_QUANT_ROWS = 4096
+
+
 def quantize_keys(K: np.ndarray, bits: int = 2):
     """Thumbnail codes, absmax and residual of every key vector (App. A; Sec. 3.1; App. C depths).
 
@@ -107,6 +110,10 @@ def quantize_keys(K: np.ndarray, bits: int = 2):
     moves it by at most ``2^-53 Q``, so the rounding is the exact one.
     """
     K = np.asarray(K, dtype=np.float64)
+    if K.ndim >= 2 and K.shape[0] > _QUANT_ROWS:
+        # rows are independent: quantize them in pieces, so the temporaries stay small
+        parts = [quantize_keys(K[i:i + _QUANT_ROWS], bits) for i in range(0, K.shape[0], _QUANT_ROWS)]
+        return tuple(np.concatenate([p[k] for p in parts]) for k in range(3))
     M = np.max(np.abs(K), axis=-1)
     Mx = M[..., None]
     u = (2 ** bits - 1) * K

@@ -1,5 +1,6 @@
 // C ABI of the FFD decode-attention library: argument checks, split choice, kernel launches.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 
@@ -11,21 +12,39 @@ using namespace ffd;
 
 namespace {
 
+// Compute units of the current device, queried once per device and cached (the only state the
+// library keeps). kFallbackCus (an MI355X's count) is used if the query fails.
+constexpr int kFallbackCus = 256;
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+
+int device_cus() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return kFallbackCus;
+    int n = g_cus[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        n = kFallbackCus;
+    g_cus[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
 // Automatic split counts. The FFD refinement grid has W + B*Hkv = (S + 1) * B*Hkv workgroups of
-// equal work; it should not exceed one per CU on the 256 CUs, because a CU serves its older
-// workgroup's memory requests first, so a second workgroup on a CU finishes its share about 3 us
-// later (at 4 x 128K, delta 5: S = 7 (256 workgroups) 60.0 us per step; S = 8 (288) 65.2 us;
-// S = 15 (512) 62.2 us; S = 6 (224) 62.3 us). The dense path keeps two workgroups per CU, its best
-// split count (S = 7 measured 1 % slower at 4 x 128K).
-constexpr int kFfdTargetWorkgroups = 256;
-constexpr int kDenseTargetWorkgroups = 512;
+// equal work; it should not exceed one per CU, because a CU serves its older workgroup's memory
+// requests first, so a second workgroup on a CU finishes its share about 3 us later (at 4 x 128K on
+// 256 CUs, delta 5: S = 7 (256 workgroups) 60.0 us per step; S = 8 (288) 65.2 us; S = 15 (512)
+// 62.2 us; S = 6 (224) 62.3 us). The dense path keeps two workgroups per CU, its best split count
+// (S = 7 measured 1 % slower at 4 x 128K).
+int ffd_target_workgroups() { return device_cus(); }
+int dense_target_workgroups() { return 2 * device_cus(); }
 constexpr int kMinBlocksPerSplit = 8;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int resolve_splits(int B, int Hkv, int Lcap, int num_splits, int target = kFfdTargetWorkgroups) {
+int resolve_splits(int B, int Hkv, int Lcap, int num_splits, bool dense = false) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
     if (num_splits > 0) return num_splits;
+    const int target = dense ? dense_target_workgroups() : ffd_target_workgroups();
     const long long pairs = (long long)B * Hkv;
     long long s = target / pairs - 1;
     const long long cap = (long long)(Lcap / FFD_BLOCK) / kMinBlocksPerSplit;
@@ -79,18 +98,18 @@ Partials carve(void* ws, int B, int Hq, int S) {
 
 int head_tiles(int G) { return G <= 4 ? 1 : 2; }
 
-// Workgroups of the scan kernel per (sequence, KV head): about kScanWorkgroups in all (one 8-wave
+// Workgroups of the scan kernel per (sequence, KV head): about one per CU in all (one 8-wave
 // workgroup per CU: 8 waves x 4 blocks of 2 KiB in flight cover a CU's share of the HBM bandwidth at
 // its load latency; 512 or 1024 workgroups of 8 or 4 waves measured 0.6-1.1 us slower at 4 x 128K),
 // each scanning at least kMinScanBlocks blocks so the pseudo-max and query setup stay a small part
 // of its work, and at most kFfdMaxScanBlocks (their maxima are staged in LDS).
-constexpr int kScanWorkgroups = 256;
 constexpr int kMinScanBlocks = 16;
 
 int scan_splits(int B, int Hkv, int Lcap) {
     const long long pairs = (long long)B * Hkv;
     const long long nblk_cap = Lcap / FFD_BLOCK;
-    long long s = (kScanWorkgroups + pairs - 1) / pairs;
+    const long long target = device_cus();
+    long long s = (target + pairs - 1) / pairs;
     const long long cap = nblk_cap / kMinScanBlocks;
     if (s > cap) s = cap;
     const long long need = (nblk_cap + kFfdMaxScanBlocks - 1) / kFfdMaxScanBlocks;
@@ -123,7 +142,7 @@ FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
 int attention_common_checks(const void* q, const void* v, const int32_t* seq_lens, int B, int Hq,
                             int Hkv, int Lcap, int D, int num_splits, float softmax_scale,
                             const void* out, const float* lse, const void* ws, size_t ws_bytes,
-                            int target, int* S_out) {
+                            bool dense, int* S_out) {
     int st = check_shapes(B, Hq, Hkv, Lcap, D);
     if (st != FFD_OK) return st;
     if (num_splits < 0 || num_splits > FFD_MAX_SPLITS) return FFD_ERR_INVALID_ARGUMENT;
@@ -133,7 +152,7 @@ int attention_common_checks(const void* q, const void* v, const int32_t* seq_len
     if (!aligned16(q) || !aligned16(v) || !aligned16(out) || !aligned16(ws)) return FFD_ERR_INVALID_ARGUMENT;
     if ((reinterpret_cast<uintptr_t>(seq_lens) & 3u) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
         return FFD_ERR_INVALID_ARGUMENT;
-    const int S = resolve_splits(B, Hkv, Lcap, num_splits, target);
+    const int S = resolve_splits(B, Hkv, Lcap, num_splits, dense);
     if (S <= 0) return FFD_ERR_INVALID_ARGUMENT;
     *S_out = S;
     return FFD_OK;
@@ -179,12 +198,12 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
 }
 
 int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
-    return resolve_splits(B, Hkv, Lcap, num_splits, kDenseTargetWorkgroups);
+    return resolve_splits(B, Hkv, Lcap, num_splits, true);
 }
 
 size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
-    const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits, kDenseTargetWorkgroups);
+    const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits, true);
     if (S <= 0) return 0;
     return partials_bytes(B, Hq, S, D);
 }
@@ -275,7 +294,7 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     int st = check_bits(thumb_bits);
     if (st != FFD_OK) return st;
     st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
-                                     lse, workspace, workspace_bytes, kFfdTargetWorkgroups, &S);
+                                     lse, workspace, workspace_bytes, false, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
     if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
@@ -351,7 +370,7 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
                                hipStream_t stream) {
     int S = 0;
     int st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
-                                     lse, workspace, workspace_bytes, kDenseTargetWorkgroups, &S);
+                                     lse, workspace, workspace_bytes, true, &S);
     if (st != FFD_OK || B == 0) return st;
     if (!k || !aligned16(k)) return FFD_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits))

@@ -3,6 +3,8 @@
 Masks must be bit-exact except blocks whose score lies within 1e-3 of the threshold (counted and
 printed); outputs and lse are compared with the oracle's attention on the GPU's own mask.
 """
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -162,23 +164,50 @@ def test_argument_errors_return_status_without_launch():
     assert e.value.status == 3
 
 
-@pytest.mark.parametrize("wl,heads", [(3, [(0, 0), (1, 3), (3, 7)]), (4, [(0, 0), (0, 5)]),
-                                      (5, [(0, 0), (1, 2), (6, 5), (15, 7)])])
-def test_full_size_workloads_sampled(wl, heads):
-    """Workloads 3-5 at full size in the benchmark's launch configuration (automatic splits);
-    masks and outputs against the oracle on sampled (sequence, KV head) pairs."""
-    c = I.workload(wl)
-    print(f"case {c.name} seed {c.seed} pairs {heads}", flush=True)
+@functools.lru_cache(maxsize=1)
+def _workload(wl):
+    return I.workload(wl)
+
+
+def _largest_planted(c, n):
+    """The n (sequence, KV head) pairs with the most planted heavy blocks: the largest unions of
+    kept blocks, chosen from the generator's structure (not from any GPU output)."""
+    return sorted(c.heavy_blocks, key=lambda bh: (-len(c.heavy_blocks[bh]), bh))[:n]
+
+
+def _full_size(wl, delta, heads):
+    c = _workload(wl)
+    heads = heads(c) if callable(heads) else heads
+    print(f"case {c.name} seed {c.seed} delta {delta} pairs {heads}", flush=True)
     up = Uploaded(c)
     qk = _quant(up)
-    out, lse, mask = _ffd(up, qk, 5.0)
-    near, flipped = compare_ffd(c, 5.0, out, lse, mask, heads=heads)
+    out, lse, mask = _ffd(up, qk, delta)
+    near, flipped = compare_ffd(c, delta, out, lse, mask, heads=heads)
     keep = mask.cpu().numpy()
-    print(f"near-threshold blocks {near}, flipped {flipped}; kept fraction {keep.mean():.4f}")
+    G = c.G
+    union = [keep[b, h * G:(h + 1) * G].any(axis=0).mean() for b, h in heads]
+    print(f"near-threshold blocks {near}, flipped {flipped}; kept head-blocks {keep.mean():.4f}; "
+          f"union keep of the checked pairs {[round(float(u), 4) for u in union]}", flush=True)
     # no head anywhere ends with an empty selection (the pseudo-max's own block always passes)
     for b, L in enumerate(c.seq_lens):
         if L > 0:
             assert keep[b].any(axis=-1).all()
+
+
+@pytest.mark.parametrize("wl,delta,heads", [
+    (3, 5.0, [(0, 0), (1, 3), (3, 7)]),
+    (3, 3.0, lambda c: _largest_planted(c, 3) + [(2, 4)]),
+    (3, 7.0, lambda c: _largest_planted(c, 3) + [(1, 1)]),
+    (4, 5.0, [(0, h) for h in range(8)]),
+    (5, 5.0, [(0, 0), (1, 2), (6, 5), (15, 7)]),
+], ids=["wl3-d5", "wl3-d3", "wl3-d7", "wl4-d5-all-heads", "wl5-d5"])
+def test_full_size_workloads_sampled(wl, delta, heads):
+    """Workloads 3-5 at full size in the benchmark's launch configuration (automatic splits);
+    masks and outputs against the oracle on sampled (sequence, KV head) pairs: at workload 3 for
+    each delta of its sweep (for 3 and 7 on the pairs with the most planted blocks, whose unions
+    are the largest), at workload 4 on all eight KV heads (the recent window's scores straddle
+    m~ - delta there)."""
+    _full_size(wl, delta, heads)
 
 
 def test_maximum_capacity():

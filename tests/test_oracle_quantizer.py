@@ -124,3 +124,17 @@ def test_residual_exhaustive_ties_to_even():
     expect = np.where(fr > 0.5, fl + 1, np.where(fr < 0.5, fl, np.where(fl % 2 == 0, fl, fl + 1)))
     assert np.array_equal(n, expect.astype(np.int64))
     assert (fr == 0.5).sum() > 0                    # the sweep does contain exact ties
+
+
+def test_quantization_in_pieces_equals_the_whole(monkeypatch):
+    """Large inputs are quantized in pieces of rows (each row independently): same results."""
+    rng = np.random.default_rng(21)
+    K = O.bf16_to_f64(O.f64_to_bf16_bits(rng.standard_normal((9000, 128)) * 3))
+    K[17] = 0.0
+    for bits in (2, 4, 8):
+        a = O.quantize_keys(K, bits)
+        monkeypatch.setattr(O, "_QUANT_ROWS", 1 << 30)
+        b = O.quantize_keys(K, bits)
+        monkeypatch.undo()
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
