@@ -70,7 +70,9 @@ typedef enum {
     FFD_ERR_INVALID_ARGUMENT = 1,    /* null/misaligned pointer, bad shape, bad delta, bad range   */
     FFD_ERR_UNSUPPORTED = 2,         /* valid but not implemented: D != 128, block != 64, G > 8    */
     FFD_ERR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes < ffd_workspace_bytes(...)                 */
-    FFD_ERR_HIP = 4                  /* a HIP launch failed (hipGetLastError after the launch)     */
+    FFD_ERR_HIP = 4,                 /* a HIP launch failed (hipGetLastError after the launch)     */
+    FFD_ERR_SCRATCH_TOO_SMALL = 5    /* ffd_decode_attention_noalloc: the call needs more workspace
+                                        than the library's fixed device scratch holds              */
 } ffd_status;
 
 #define FFD_HEAD_DIM 128
@@ -195,6 +197,27 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
                             void* out, float* lse, uint8_t* block_mask,
                             void* workspace, size_t workspace_bytes, hipStream_t stream,
                             const ffd_decode_extras* extras);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): ffd_decode_attention without a workspace argument. The
+ * workspace is a fixed device array of FFD_NOALLOC_SCRATCH_BYTES inside the library, one per device,
+ * which the device holds from the first call on it until the process ends (that first call resolves
+ * its address; no call allocates). Arguments, outputs and kernels are those of ffd_decode_attention.
+ *  - A call whose ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits) exceeds the scratch returns
+ *    FFD_ERR_SCRATCH_TOO_SMALL before any launch (16 MiB covers, for example, B * Hkv = 128 KV
+ *    groups at Lcap = 131072 and G = 4).
+ *  - Every call on a device uses that device's one scratch array, and the array keeps the last
+ *    call's contents (nothing in it needs to start at zero). Calls that overlap in time on one
+ *    device (different streams, or different host threads) race on it and give undefined results:
+ *    serialise them, or use ffd_decode_attention with separate workspaces.
+ */
+#define FFD_NOALLOC_SCRATCH_BYTES (16u << 20)
+int ffd_decode_attention_noalloc(const void* q, const void* k_codes, const void* k_absmax,
+                                 const void* k_resid, const void* v, const int32_t* seq_lens,
+                                 int B, int Hq, int Hkv, int Lcap, int D, int thumb_bits, int block_size,
+                                 float delta, int n_sink, int n_local, int num_splits, float softmax_scale,
+                                 void* out, float* lse, uint8_t* block_mask, hipStream_t stream);
 
 /*
  * Exact dense decode attention over bf16 keys and values (the FlashAttention-2 comparator of

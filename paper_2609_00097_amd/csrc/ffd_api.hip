@@ -3,6 +3,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "ffd.h"
 #include "ffd_device.h"
@@ -27,6 +28,29 @@ int device_cus() {
         n = kFallbackCus;
     g_cus[dev].store(n, std::memory_order_relaxed);
     return n;
+}
+
+// Device scratch of ffd_decode_attention_noalloc: one array per device, held until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: the array is only ever
+// reached through the address hipGetSymbolAddress returns for the current device, cached per device.
+constexpr size_t kNoallocScratchBytes = (size_t)FFD_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// The current device's scratch address (resolved on the first call on that device), or null.
+void* device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    void* p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch[dev].store(p, std::memory_order_release);
+    }
+    return p;
 }
 
 // Automatic split counts. The FFD refinement grid has W + B*Hkv = (S + 1) * B*Hkv workgroups of
@@ -142,14 +166,15 @@ FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
 int attention_common_checks(const void* q, const void* v, const int32_t* seq_lens, int B, int Hq,
                             int Hkv, int Lcap, int D, int num_splits, float softmax_scale,
                             const void* out, const float* lse, const void* ws, size_t ws_bytes,
-                            bool dense, int* S_out) {
+                            bool dense, int* S_out, bool check_ws = true) {
     int st = check_shapes(B, Hq, Hkv, Lcap, D);
     if (st != FFD_OK) return st;
     if (num_splits < 0 || num_splits > FFD_MAX_SPLITS) return FFD_ERR_INVALID_ARGUMENT;
     if (!(softmax_scale >= 0.f) || std::isinf(softmax_scale)) return FFD_ERR_INVALID_ARGUMENT;
     if (B == 0) { *S_out = 0; return FFD_OK; }
-    if (!q || !v || !seq_lens || !out || !ws) return FFD_ERR_INVALID_ARGUMENT;
-    if (!aligned16(q) || !aligned16(v) || !aligned16(out) || !aligned16(ws)) return FFD_ERR_INVALID_ARGUMENT;
+    if (!q || !v || !seq_lens || !out || (check_ws && !ws)) return FFD_ERR_INVALID_ARGUMENT;
+    if (!aligned16(q) || !aligned16(v) || !aligned16(out) || (check_ws && !aligned16(ws)))
+        return FFD_ERR_INVALID_ARGUMENT;
     if ((reinterpret_cast<uintptr_t>(seq_lens) & 3u) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
         return FFD_ERR_INVALID_ARGUMENT;
     const int S = resolve_splits(B, Hkv, Lcap, num_splits, dense);
@@ -189,6 +214,35 @@ void launch_refine_nt(int rbits, dim3 grid, hipStream_t stream, const RefineArgs
     else hipLaunchKernelGGL((ffd_refine_kernel<NT, 8>), grid, dim3(kThreads), 0, stream, ra);
 }
 
+// Every argument check of ffd_decode_attention_ex, in its order, with nothing launched; with
+// check_ws false the workspace pointer is not checked (the no-alloc entry point brings its own).
+// *S_out receives the split count (0 when B == 0).
+int decode_checks(const void* q, const void* k_codes, const void* k_absmax, const void* k_resid,
+                  const void* v, const int32_t* seq_lens, int B, int Hq, int Hkv, int Lcap, int D,
+                  int thumb_bits, int block_size, float delta, int n_sink, int n_local, int num_splits,
+                  float softmax_scale, const void* out, const float* lse, const void* workspace,
+                  const ffd_decode_extras* extras, bool check_ws, int* S_out) {
+    const float* m_tilde = extras ? extras->m_tilde : nullptr;
+    const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
+    const int top_k = extras ? extras->top_k : 0;
+    if (pm_source != FFD_PSEUDO_MAX_THUMBNAIL && pm_source != FFD_PSEUDO_MAX_REFINED)
+        return FFD_ERR_INVALID_ARGUMENT;
+    if (top_k < 0 || (top_k > 0 && m_tilde)) return FFD_ERR_INVALID_ARGUMENT;
+    if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
+    if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
+    int st = check_bits(thumb_bits);
+    if (st != FFD_OK) return st;
+    st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
+                                 lse, workspace, 0, false, S_out, check_ws);
+    if (st != FFD_OK || B == 0) return st;
+    if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
+    if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
+    if (m_tilde && (reinterpret_cast<uintptr_t>(m_tilde) & 3u)) return FFD_ERR_INVALID_ARGUMENT;
+    if ((long long)B * Hkv > (1LL << 20)) return FFD_ERR_UNSUPPORTED;
+    if (Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return FFD_ERR_UNSUPPORTED;
+    return FFD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -224,6 +278,7 @@ const char* ffd_status_string(int status) {
         case FFD_ERR_UNSUPPORTED: return "FFD_ERR_UNSUPPORTED";
         case FFD_ERR_WORKSPACE_TOO_SMALL: return "FFD_ERR_WORKSPACE_TOO_SMALL";
         case FFD_ERR_HIP: return "FFD_ERR_HIP";
+        case FFD_ERR_SCRATCH_TOO_SMALL: return "FFD_ERR_SCRATCH_TOO_SMALL";
         default: return "FFD_ERR_UNKNOWN";
     }
 }
@@ -285,22 +340,11 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     float* m_tilde = extras ? extras->m_tilde : nullptr;
     const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
     const int top_k = extras ? extras->top_k : 0;
-    if (pm_source != FFD_PSEUDO_MAX_THUMBNAIL && pm_source != FFD_PSEUDO_MAX_REFINED)
-        return FFD_ERR_INVALID_ARGUMENT;
-    if (top_k < 0 || (top_k > 0 && m_tilde)) return FFD_ERR_INVALID_ARGUMENT;
-    if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
-    if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
     int S = 0;
-    int st = check_bits(thumb_bits);
-    if (st != FFD_OK) return st;
-    st = attention_common_checks(q, v, seq_lens, B, Hq, Hkv, Lcap, D, num_splits, softmax_scale, out,
-                                     lse, workspace, workspace_bytes, false, &S);
+    int st = decode_checks(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D, thumb_bits,
+                           block_size, delta, n_sink, n_local, num_splits, softmax_scale, out, lse,
+                           workspace, extras, true, &S);
     if (st != FFD_OK || B == 0) return st;
-    if (!k_codes || !k_absmax || !k_resid) return FFD_ERR_INVALID_ARGUMENT;
-    if (!aligned16(k_codes) || !aligned16(k_absmax) || !aligned16(k_resid)) return FFD_ERR_INVALID_ARGUMENT;
-    if (m_tilde && (reinterpret_cast<uintptr_t>(m_tilde) & 3u)) return FFD_ERR_INVALID_ARGUMENT;
-    if ((long long)B * Hkv > (1LL << 20)) return FFD_ERR_UNSUPPORTED;
-    if (Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return FFD_ERR_UNSUPPORTED;
     if (workspace_bytes < ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)) return FFD_ERR_WORKSPACE_TOO_SMALL;
     const int G = Hq / Hkv;
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
@@ -362,6 +406,25 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
     return ffd_decode_attention_ex(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
                                    thumb_bits, block_size, delta, n_sink, n_local, num_splits, softmax_scale, out,
                                    lse, block_mask, workspace, workspace_bytes, stream, nullptr);
+}
+
+int ffd_decode_attention_noalloc(const void* q, const void* k_codes, const void* k_absmax,
+                                 const void* k_resid, const void* v, const int32_t* seq_lens, int B, int Hq,
+                                 int Hkv, int Lcap, int D, int thumb_bits, int block_size, float delta,
+                                 int n_sink, int n_local, int num_splits, float softmax_scale, void* out,
+                                 float* lse, uint8_t* block_mask, hipStream_t stream) {
+    int S = 0;
+    const int st = decode_checks(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D, thumb_bits,
+                                 block_size, delta, n_sink, n_local, num_splits, softmax_scale, out, lse,
+                                 nullptr, nullptr, false, &S);
+    if (st != FFD_OK || B == 0) return st;
+    if (ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits) > kNoallocScratchBytes)
+        return FFD_ERR_SCRATCH_TOO_SMALL;
+    void* ws = device_scratch();
+    if (!ws) return FFD_ERR_HIP;
+    return ffd_decode_attention_ex(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D,
+                                   thumb_bits, block_size, delta, n_sink, n_local, num_splits, softmax_scale,
+                                   out, lse, block_mask, ws, kNoallocScratchBytes, stream, nullptr);
 }
 
 int ffd_dense_decode_attention(const void* q, const void* k, const void* v, const int32_t* seq_lens, int B,

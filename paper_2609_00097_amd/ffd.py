@@ -20,10 +20,11 @@ BLOCK = 64
 MAX_SPLITS = 1024
 THUMB_BITS = (2, 4, 8)      # thumbnail depths: 2+8 (the method), 4+8 and 8+8 (App. C)
 STATUS = {0: "FFD_OK", 1: "FFD_ERR_INVALID_ARGUMENT", 2: "FFD_ERR_UNSUPPORTED",
-          3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP"}
+          3: "FFD_ERR_WORKSPACE_TOO_SMALL", 4: "FFD_ERR_HIP", 5: "FFD_ERR_SCRATCH_TOO_SMALL"}
+NOALLOC_SCRATCH_BYTES = 16 << 20     # FFD_NOALLOC_SCRATCH_BYTES
 
 EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
-           "ffd_dense_decode_attention",
+           "ffd_decode_attention_noalloc", "ffd_dense_decode_attention",
            "ffd_resolve_splits", "ffd_dense_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
 
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
     so.ffd_decode_attention.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, F, I, I, I, F,
                                         P, P, P, P, SZ, P]
     so.ffd_decode_attention_ex.argtypes = so.ffd_decode_attention.argtypes + [ctypes.POINTER(DecodeExtras)]
+    so.ffd_decode_attention_noalloc.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, F, I, I, I, F,
+                                                P, P, P, P]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
     so.ffd_resolve_splits.argtypes = [I, I, I, I]
     so.ffd_dense_resolve_splits.argtypes = [I, I, I, I]
@@ -75,7 +78,8 @@ def lib() -> ctypes.CDLL:
     so.ffd_status_string.argtypes = [I]
     so.ffd_status_string.restype = ctypes.c_char_p
     for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
-                 "ffd_dense_decode_attention", "ffd_resolve_splits", "ffd_dense_resolve_splits"):
+                 "ffd_decode_attention_noalloc", "ffd_dense_decode_attention", "ffd_resolve_splits",
+                 "ffd_dense_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
     return so
@@ -253,6 +257,33 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
         D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
         _ptr(lse), _ptr(mask), _ptr(workspace), workspace.numel() * workspace.element_size(),
         _stream(q.device), ctypes.byref(extras)))
+    return out, lse, mask
+
+
+def decode_attention_noalloc(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_sink: int = 64,
+                             n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
+                             out=None, lse=None, mask=None):
+    """``decode_attention`` through ``ffd_decode_attention_noalloc``: the library's fixed device
+    scratch stands in for the workspace (no device allocation by the library; calls on one device
+    must not overlap in time). ``out`` (and ``lse``/``mask`` when wanted) should be passed in by
+    callers that cannot allocate; otherwise they are allocated here. Returns ``(out, lse, mask)``."""
+    B, Hq, D = q.shape
+    Hkv, Lcap = v.shape[1], v.shape[2]
+    _need(q, "q", torch.bfloat16)
+    _need(v, "v", torch.bfloat16, (B, Hkv, Lcap, D))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    bits = _need_quantized((codes, absmax, resid), B, Hkv, Lcap)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=torch.bfloat16, device=q.device)
+    _need(out, "out", torch.bfloat16, (B, Hq, D))
+    if lse is not None:
+        _need(lse, "lse", torch.float32, (B, Hq))
+    if mask is not None:
+        _need(mask, "mask", torch.uint8, (B, Hq, Lcap // BLOCK))
+    _check("ffd_decode_attention_noalloc", lib().ffd_decode_attention_noalloc(
+        _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
+        D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),
+        _ptr(lse), _ptr(mask), _stream(q.device)))
     return out, lse, mask
 
 
