@@ -92,8 +92,10 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(case, mask, S, bits=2):
-    """Bytes one FFD step must move, counted from the measured per-head block mask (b-bit codes)."""
+def algorithmic_bytes(case, mask, rows, bits=2):
+    """Bytes one FFD step must move, counted from the measured per-head block mask (b-bit codes).
+    ``rows`` partial states per head are written and then merged (0: the kernel writes the outputs
+    itself)."""
     G, D = case.G, case.D
     scan_per_token = SCAN_BYTES_PER_TOKEN + 16 * (bits - 2)
     scan = 0
@@ -110,7 +112,7 @@ def algorithmic_bytes(case, mask, S, bits=2):
             gather_tokens += int(toks.sum())
     gather = GATHER_BYTES_PER_TOKEN * gather_tokens
     io = case.B * case.Hq * (2 * D + 2 * D + 4)                  # q in, out, lse
-    partials = 2 * case.B * case.Hq * (S + 1) * (D + 2) * 4        # (S + 1) rows per head, written, then merged
+    partials = 2 * case.B * case.Hq * rows * (D + 2) * 4             # written, then merged
     return dict(scan=scan, gather=gather, io=io, partials=partials,
                 total=scan + gather + io + partials, gather_tokens=gather_tokens)
 
@@ -119,6 +121,28 @@ def dense_bytes(case, S):
     tok = int(np.sum(case.seq_lens)) * case.Hkv
     return DENSE_BYTES_PER_TOKEN * tok + case.B * case.Hq * (4 * case.D + 4) + \
         2 * case.B * case.Hq * S * (case.D + 2) * 4
+
+
+def partial_rows(r, kernels):
+    """Partial states per head of a step with these kernels: the fused kernel's S1 (none when
+    S1 == 1), or about S + 1 for the split kernels (W + B*Hkv refinement workgroups over the groups)."""
+    if kernels == "fused":
+        s1 = r.ffd.fused_splits(r.case.B, r.case.Hkv, r.case.Lcap, r.splits)
+        return s1 if s1 > 1 else 0
+    return r.S + 1
+
+
+def stage_table(kernels, nbytes, case):
+    """Kernel names and algorithmic bytes per launch for the three stage intervals the library
+    records (the fused kernel's second interval is empty)."""
+    q = case.B * case.Hq * 2 * case.D
+    io = case.B * case.Hq * (2 * case.D + 4)
+    half = nbytes["partials"] // 2
+    if kernels == "fused":
+        return ["ffd_decode_kernel", None, "lse_merge_kernel"], \
+               [nbytes["scan"] + nbytes["gather"] + q + half, 0, half + io if half else 0]
+    return ["ffd_scan_kernel", "ffd_refine_kernel", "lse_merge_kernel"], \
+           [nbytes["scan"] + q, nbytes["gather"] + half, half + io]
 
 
 HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000    # hipEventDisableSystemFence, hip_runtime_api.h
@@ -361,13 +385,19 @@ class Runner:
         self.torch.sum(self.flush_buf)
 
     def ffd_step(self, delta, layer=0, events=None, mask=None, top_k=0, pseudo_max="thumbnail",
-                 m_tilde=None):
+                 m_tilde=None, kernels="auto"):
         c = self.case
         self.ffd.decode_attention(self.q, *self.qk[layer], self.v[layer], self.lens, delta=delta,
                                   n_sink=c.n_sink, n_local=c.n_local, num_splits=self.splits,
                                   workspace=self.ws, out=self.out, lse=self.lse, mask=mask,
                                   stage_events=events, top_k=top_k, pseudo_max=pseudo_max,
-                                  m_tilde=m_tilde)
+                                  m_tilde=m_tilde, kernels=kernels)
+
+    @property
+    def kernels(self):
+        """The top-delta kernels the library picks automatically for this case."""
+        c = self.case
+        return self.ffd.select_kernels(c.B, c.Hkv, c.Lcap, self.splits)
 
     def dense_step(self, layer=0):
         self.ffd.dense_decode_attention(self.q, self.k[layer], self.v[layer], self.lens,
@@ -481,14 +511,16 @@ def depth_sweep(r, delta, depths, steps, dense_us):
         for layer in range(r.n_layers):
             ffd.quantize_keys(r.k[layer], out=r.qk[layer])
         keep = r.mask_for(delta)
-        nb = algorithmic_bytes(c, keep, r.S, bits)
+        kern = r.kernels
+        nb = algorithmic_bytes(c, keep, partial_rows(r, kern), bits)
         us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
         su = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev), steps).mean(axis=0)
-        scan_bytes = nb["scan"] + c.B * c.Hq * 2 * c.D
-        out[f"{bits}+8"] = {"us": round(us, 2), "scan_us": round(float(su[0]), 2),
-                            "refine_us": round(float(su[1]), 2), "merge_us": round(float(su[2]), 2),
-                            "scan_bytes": int(scan_bytes),
-                            "scan_gbps": round(scan_bytes / (float(su[0]) * 1e-6) / 1e9, 1),
+        names, sbytes = stage_table(kern, nb, c)
+        out[f"{bits}+8"] = {"us": round(us, 2), "kernels": kern,
+                            "stages_us": {k: round(float(u), 2) for k, u in zip(names, su) if k},
+                            "stages_gbps": {k: round(bb / (float(u) * 1e-6) / 1e9, 1)
+                                            for k, u, bb in zip(names, su, sbytes) if k and u > 0},
+                            "scan_bytes": int(nb["scan"]), "gather_bytes": int(nb["gather"]),
                             "keep_head_blocks": round(float(keep.mean()), 5),
                             "speedup_vs_dense": round(dense_us / us, 2)}
     r.qk = None
@@ -505,7 +537,7 @@ def selection_rule(r, delta, keep, steps, dense_us, stage_us, td_us):
     kept = sum(int(keep[b, :, :nb[b]].sum()) for b in range(c.B))
     k = max(1, int(round(kept / float(c.B * c.Hq))))
     kk = r.mask_for(delta, top_k=k)
-    bk = algorithmic_bytes(c, kk, r.S)
+    bk = algorithmic_bytes(c, kk, r.S + 1)
     us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer, top_k=k), steps, 5)
     su = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev, top_k=k), steps).mean(axis=0)
     ratio = lambda m: float(np.mean(np.concatenate([m[b, :, :nb[b]].ravel() for b in range(c.B)])))
@@ -515,13 +547,13 @@ def selection_rule(r, delta, keep, steps, dense_us, stage_us, td_us):
             "top_k_keep_union_tokens": round(bk["gather_tokens"] / float(c.seq_lens.sum() * c.Hkv), 5),
             "top_k_stages_us": {"scan_and_select": round(float(su[0]), 2), "refine": round(float(su[1]), 2),
                                 "merge": round(float(su[2]), 2)},
-            "top_delta_stages_us": {"scan_and_select": round(float(stage_us[0]), 2),
-                                    "refine": round(float(stage_us[1]), 2), "merge": round(float(stage_us[2]), 2)},
+            "top_delta_stages_us": stage_us,
             "top_k_speedup_vs_dense": round(dense_us / us, 2),
             "what": "top-k keeps per head the k blocks with the largest thumbnail block scores (scan, "
                     "then a per-(sequence, KV head) radix-select kernel, then the refinement recomputing "
-                    "the kept blocks' thumbnail scores); k = top-delta's mean kept blocks per head at "
-                    "this delta; layer-averaged protocol; stage times from library events in separate steps"}
+                    "the kept blocks' thumbnail scores, then the merge), against top-delta's kernels; "
+                    "k = top-delta's mean kept blocks per head at this delta; layer-averaged protocol; "
+                    "stage times from library events in separate steps"}
 
 
 def exact_max(r):
@@ -597,10 +629,16 @@ def context_sweep(lengths_k, splits, flush_mib, delta, steps, layers):
         case = I.context_case(lk * 1024)
         r = Runner(case, splits, flush_mib, layers)
         keep = r.mask_for(delta)
-        nb = algorithmic_bytes(case, keep, r.S)
+        kern = r.kernels
+        nb = algorithmic_bytes(case, keep, partial_rows(r, kern))
         f_us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
+        by_kernels = {}
+        for kk in ("fused", "split"):
+            u, _ = r.rotate(lambda layer: r.ffd_step(delta, layer, kernels=kk), steps, 5)
+            by_kernels[kk] = round(u, 2)
         d_us, _ = r.rotate(r.dense_step, steps, 5)
-        out[f"{lk}K"] = {"ffd_us": round(f_us, 2), "dense_us": round(d_us, 2),
+        out[f"{lk}K"] = {"ffd_us": round(f_us, 2), "kernels": kern, "ffd_us_by_kernels": by_kernels,
+                         "dense_us": round(d_us, 2),
                          "speedup_vs_dense": round(d_us / f_us, 2),
                          "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
                          "dense_tbps": round(dense_bytes(case, r.Sd) / (d_us * 1e-6) / 1e12, 3),
@@ -626,11 +664,17 @@ def workload_sweep(splits, flush_mib, steps, layers):
                  "dense_tbps": round(dense_bytes(case, r.Sd) / (d_us * 1e-6) / 1e12, 3)}
         for delta in case.deltas:
             keep = r.mask_for(delta)
-            nb = algorithmic_bytes(case, keep, r.S)
+            kern = r.kernels
+            nb = algorithmic_bytes(case, keep, partial_rows(r, kern))
             f_us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer), steps, 5)
+            by_kernels = {}
+            for kk in ("fused", "split"):
+                u, _ = r.rotate(lambda layer: r.ffd_step(delta, layer, kernels=kk), steps, 5)
+                by_kernels[kk] = round(u, 2)
             valid = np.concatenate([keep[b, :, :-(-int(case.seq_lens[b]) // 64)].ravel() for b in range(case.B)])
             entry[f"delta={delta:g}"] = {
-                "ffd_us": round(f_us, 2), "speedup_vs_dense": round(d_us / f_us, 2),
+                "ffd_us": round(f_us, 2), "kernels": kern, "ffd_us_by_kernels": by_kernels,
+                "speedup_vs_dense": round(d_us / f_us, 2),
                 "ffd_tbps": round(nb["total"] / (f_us * 1e-6) / 1e12, 3),
                 "keep_head_blocks": round(float(valid.mean()), 5),
                 "keep_union_tokens": round(nb["gather_tokens"] / float(case.seq_lens.sum() * case.Hkv), 5)}
@@ -658,12 +702,13 @@ def main():
     case = I.workload(args.workload)
     log(f"uploading {args.layers} cache copies and quantizing")
     r = Runner(case, args.splits, args.flush_mib, args.layers)
-    S = r.S
     delta = args.delta
+    kern = r.kernels
+    rows = partial_rows(r, kern)
 
     # the measured mask gives the algorithmic bytes (mask output off in the timed steps)
     keep = r.mask_for(delta)
-    nbytes = algorithmic_bytes(case, keep, S)
+    nbytes = algorithmic_bytes(case, keep, rows)
 
     ffd_fn = lambda layer: r.ffd_step(delta, layer)        # noqa: E731
     log("timing the FFD step (layer-averaged)")
@@ -696,6 +741,11 @@ def main():
     # markers between kernels add a few microseconds of gap, so these steps are not the headline
     stage_us = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev),
                                max(16, args.steps // 2)).mean(axis=0)
+    # the other kernels on the same workload, for comparison
+    other = "split" if kern == "fused" else "fused"
+    other_us, _ = r.rotate(lambda layer: r.ffd_step(delta, layer, kernels=other), 32, 4)
+    other_st = r.rotate_stages(lambda layer, ev: r.ffd_step(delta, layer, events=ev, kernels=other), 16).mean(axis=0)
+    other_names, _ = stage_table(other, nbytes, case)
 
     # dense flash-decode baseline, same protocol
     dense_us, _ = r.rotate(r.dense_step, args.dense_steps, 4)
@@ -709,29 +759,34 @@ def main():
     sweep = {}
     for d in [float(x) for x in args.sweep_deltas.split(",") if x.strip()]:
         kd = r.mask_for(d)
-        bd = algorithmic_bytes(case, kd, S)
+        bd = algorithmic_bytes(case, kd, rows)
         su, _ = r.rotate(lambda layer: r.ffd_step(d, layer), 24, 4)
         ss = r.rotate_stages(lambda layer, ev: r.ffd_step(d, layer, events=ev), 16).mean(axis=0)
+        names, sbytes = stage_table(kern, bd, case)
         sweep[str(d)] = {"us": round(su, 2), "tbps": round(bd["total"] / (su * 1e-6) / 1e12, 3),
                          "keep_head_blocks": round(float(kd.mean()), 5),
                          "keep_union_tokens": round(bd["gather_tokens"] / float(np.sum(case.seq_lens) * case.Hkv), 5),
-                         "stages_us": [round(float(x), 2) for x in ss],
-                         "refine_gbps": round(bd["gather"] / (float(ss[1]) * 1e-6) / 1e9, 1),
+                         "stages_us": {k: round(float(u), 2) for k, u in zip(names, ss) if k},
+                         "stages_gbps": {k: round(bb / (float(u) * 1e-6) / 1e9, 1)
+                                         for k, u, bb in zip(names, ss, sbytes) if k and u > 0},
                          "speedup_vs_dense": round(dense_us / su, 2)}
 
     log("selection rule, copy ceiling, depth sweep, fidelity, decode loop")
-    selection = selection_rule(r, delta, keep, 32, dense_us, stage_us, eager_us)
+    names, sbytes = stage_table(kern, nbytes, case)
+    stage_dict = {k: round(float(u), 2) for k, u in zip(names, stage_us) if k}
+    selection = selection_rule(r, delta, keep, 32, dense_us, stage_dict, eager_us)
     ceiling = stream_ceiling(r)
     depths = depth_sweep(r, delta, [int(x) for x in args.depths.split(",") if x.strip()],
                          24, dense_us)
     fid = None if args.no_fidelity else fidelity(r, [3.0, 5.0, 7.0], 24)
     loop = decode_loop(r, delta, min(args.steps, 48), 8)      # writes the caches: run last
 
-    # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration
-    stage_bytes = {"ffd_scan_kernel": nbytes["scan"] + case.B * case.Hq * 2 * case.D,
-                   "ffd_refine_kernel": nbytes["gather"],
-                   "lse_merge_kernel": nbytes["partials"] // 2 + case.B * case.Hq * (2 * case.D + 4)}
+    # roofline of the dominant kernel: its algorithmic bytes / its event-timed duration (the scan
+    # kernel moves codes + absmax of every token and the queries, the refinement the residual +
+    # values of the union-kept tokens and its partials, the fused kernel both)
+    stage_bytes = {k: bb for k, bb in zip(names, sbytes) if k}
     names = list(stage_bytes)
+    stage_us = np.array([u for k, u in zip(stage_table(kern, nbytes, case)[0], stage_us) if k])
     dom = names[int(np.argmax(stage_us))]
     dom_us = float(stage_us[names.index(dom)])
     dom_gbps = stage_bytes[dom] / (dom_us * 1e-6) / 1e9
@@ -756,7 +811,10 @@ def main():
         "config": {"workload": case.name, "batch": case.B, "context": int(case.Lcap),
                    "q_heads": case.Hq, "kv_heads": case.Hkv, "head_dim": case.D, "kv_block": 64,
                    "delta": delta, "n_sink": case.n_sink, "n_local": case.n_local,
-                   "num_splits": S, "io": "q/v/out bf16, k as 2-bit codes + int8 residual",
+                   "kernels": kern,
+                   "num_splits": r.ffd.fused_splits(case.B, case.Hkv, case.Lcap, args.splits)
+                   if kern == "fused" else r.S,
+                   "io": "q/v/out bf16, k as 2-bit codes + int8 residual",
                    "launch": "hip graph replay" if args.graph else "direct (stream-ordered) launches",
                    "protocol": f"layer-averaged: {args.layers} distinct caches, steps back to back, "
                                f"step i on cache i mod {args.layers}",
@@ -772,17 +830,17 @@ def main():
         "dense_us": round(dense_us, 2),
         "dense_tbps": round(dbytes / (dense_us * 1e-6) / 1e12, 3),
         "speedup_vs_dense": round(dense_us / us, 2),
+        "other_kernels": {"kernels": other, "us": round(other_us, 2),
+                          "stages_us": {k: round(float(u), 2) for k, u in zip(other_names, other_st) if k}},
         "flush_protocol": {
             "what": f"one cache, an untimed {args.flush_mib} MiB read before every step (event-timed "
                     "per step); part of the kept blocks stay in the Infinity Cache across steps",
             "ffd_us": round(flush_us, 2), "dense_us": round(dense_flush_us, 2),
             "effective_tbps": round(nbytes["total"] / (flush_us * 1e-6) / 1e12, 3),
-            "stages_us": {k: round(float(u), 2) for k, u in zip(("scan", "refine", "merge"), flush_stage_us)},
+            "stages_us": {k: round(float(u), 2) for k, u in zip(stage_table(kern, nbytes, case)[0], flush_stage_us) if k},
             "speedup_vs_dense": round(dense_flush_us / flush_us, 2)},
         "delta_sweep": sweep,
-        "depth_sweep": {"2+8": {"us": round(eager_us, 2), "scan_us": round(float(stage_us[0]), 2),
-                                "refine_us": round(float(stage_us[1]), 2),
-                                "merge_us": round(float(stage_us[2]), 2)}, **depths},
+        "depth_sweep": {"2+8": {"us": round(eager_us, 2), "kernels": kern, "stages_us": stage_dict}, **depths},
         "selection_rule": selection,
         "stream_ceiling": ceiling,
         "fidelity": fid,

@@ -159,12 +159,24 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
 #define FFD_PSEUDO_MAX_REFINED 1     /* m~ over their refined logits, thumbnail + residual (Eq. 3's
                                         window scores read with the 8-bit residual, Eq. 4) */
 
+/* Kernels of the top-delta rule (ffd_decode_extras.kernels). */
+#define FFD_KERNELS_AUTO 0    /* FFD_KERNELS_FUSED while each of its workgroups covers at most 64 blocks
+                                 of the capacity (ffd_select_kernels), else FFD_KERNELS_SPLIT */
+#define FFD_KERNELS_FUSED 1   /* one kernel: each of S1 = ffd_fused_splits(...) workgroups per
+                                 (sequence, KV head) scans the blocks j = s + S1 i, decides, refines and
+                                 attends its own kept blocks; then the merge of the S1 partial states
+                                 per head (no merge when S1 == 1: the kernel writes the outputs) */
+#define FFD_KERNELS_SPLIT 2   /* scan + selection kernel (contiguous block ranges), refinement kernel
+                                 (the kept blocks of all groups spread evenly over about one
+                                 workgroup per CU), merge */
+
 /*
  * Optional inputs and outputs of ffd_decode_attention_ex, for measurement and diagnostics
  * (Sec. 5.1, Sec. 5.2). A NULL pointer field, or a NULL extras pointer, leaves that feature off.
- *   stage_events  four events created by the caller (hipEventCreate), recorded on `stream` before
- *                 the scan kernel, between scan and refinement, between refinement and merge, and
- *                 after the merge.
+ *   stage_events  four events created by the caller (hipEventCreate), recorded on `stream`: before
+ *                 the first kernel; after the selection (the scan kernel, or the top-k selection
+ *                 kernel; with the fused kernel: after it); after the refinement (with the fused
+ *                 kernel: the same point); after the merge (the same point again when no merge runs).
  *   m_tilde       float [B, Hq] (device): the pseudo-max m~ of each head (-inf for an empty
  *                 sequence or when both windows are empty), for the gap m - m~ of Sec. 5.2.
  *   pseudo_max    FFD_PSEUDO_MAX_THUMBNAIL or FFD_PSEUDO_MAX_REFINED (other values:
@@ -184,6 +196,8 @@ typedef struct ffd_decode_extras {
     float* m_tilde;
     int pseudo_max;
     int top_k;
+    int kernels;        /* FFD_KERNELS_AUTO, _FUSED or _SPLIT (top-delta only; with top_k > 0 the
+                           split kernels run and FFD_KERNELS_FUSED is FFD_ERR_INVALID_ARGUMENT) */
 } ffd_decode_extras;
 
 /*
@@ -236,6 +250,16 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
  * query fails). The workspace size depends on it, so size and call on the same device.
  * 0 on invalid input. */
 int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
+
+/* Workgroups per (sequence, KV head) of the fused top-delta kernel for this num_splits: num_splits
+ * itself, or automatically about one workgroup per compute unit in all (floor) with at least 64
+ * blocks of the capacity each; raised to ceil((Lcap / 64) / 256) when smaller (a workgroup covers at
+ * most 256 blocks). 0 on invalid input. */
+int ffd_fused_splits(int B, int Hkv, int Lcap, int num_splits);
+
+/* The kernels FFD_KERNELS_AUTO uses for these arguments: FFD_KERNELS_FUSED or FFD_KERNELS_SPLIT;
+ * 0 on invalid input. */
+int ffd_select_kernels(int B, int Hkv, int Lcap, int num_splits);
 
 /* The same for ffd_dense_decode_attention, whose automatic count allows two workgroups per compute
  * unit (B * Hkv * S). */

@@ -142,19 +142,56 @@ int scan_splits(int B, int Hkv, int Lcap) {
     return (int)s;
 }
 
-// FFD workspace: partials for W + B*Hkv refinement workgroups (W = S * B * Hkv) of G heads each,
-// the per-group (first workgroup, count) table, the scan's per-split kept counts and kept lists,
-// and the block scores [P, C, G] that the top-k rule selects from.
+// Workgroups per (sequence, KV head) of the fused top-delta kernel, S1: num_splits when given,
+// else about one 8-wave workgroup per CU in all (floor, so that the grid fits one round of
+// workgroups), each with at least kMinFusedBlocks blocks of the capacity (a short context takes
+// one workgroup per group, which then writes the outputs itself, with no merge launch); never fewer
+// than ceil(blocks / kFfdMaxScanBlocks) (a workgroup's block scores are staged in LDS).
+constexpr int kMinFusedBlocks = 64;
+
+int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
+    if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
+    const long long pairs = (long long)B * Hkv;
+    const long long nblk_cap = Lcap / FFD_BLOCK;
+    const long long need = (nblk_cap + kFfdMaxScanBlocks - 1) / kFfdMaxScanBlocks;
+    long long s = num_splits;
+    if (s == 0) {
+        s = device_cus() / pairs;
+        const long long cap = nblk_cap / kMinFusedBlocks;
+        if (s > cap) s = cap;
+    }
+    if (s < need) s = need;
+    if (s < 1) s = 1;
+    if (s > kFfdMaxScanSplits) return 0;
+    return (int)s;
+}
+
+// The top-delta kernels FFD_KERNELS_AUTO picks: the fused kernel while each of its workgroups covers
+// at most kFusedMaxBlocks blocks of the capacity (its refinement, at the end of each workgroup's
+// scan, then stays short), else scan + refinement + merge, whose refinement spreads the kept blocks
+// evenly over every CU.
+constexpr int kFusedMaxBlocks = 64;
+
+int auto_kernels(int Lcap, int S1f) {
+    const int bps = (Lcap / FFD_BLOCK + S1f - 1) / S1f;
+    return bps <= kFusedMaxBlocks ? FFD_KERNELS_FUSED : FFD_KERNELS_SPLIT;
+}
+
+// FFD workspace: partial states (for the fused top-delta kernel's B * Hq * S1f rows, or for the
+// top-k path's W + B*Hkv refinement workgroups (W = S * B * Hkv) of G heads each), and for the
+// top-k path the per-group (first workgroup, count) table, the scan's per-split kept counts and
+// kept lists, and the block scores [P, C, G] it selects from.
 struct FfdWorkspace {
     size_t rows;                      // partial rows
     size_t table_off, counts_off, lists_off, sigma_off, total;
 };
 
-FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S) {
+FfdWorkspace ffd_layout(int B, int Hq, int Hkv, int Lcap, int D, int S, int S1f) {
     FfdWorkspace w;
     const size_t pairs = (size_t)B * Hkv;
     const size_t nblk_cap = (size_t)(Lcap / FFD_BLOCK);
-    w.rows = ((size_t)S * pairs + pairs) * (size_t)(Hq / Hkv);
+    // the top-k path's refinement rows, or the fused kernel's [B, Hq, S1f] rows
+    w.rows = std::max(((size_t)S * pairs + pairs) * (size_t)(Hq / Hkv), (size_t)B * Hq * (size_t)S1f);
     w.table_off = round_up(w.rows * (D + 2) * sizeof(float), kAlign);
     w.counts_off = w.table_off + round_up(pairs * 2 * sizeof(int), kAlign);
     w.lists_off = w.counts_off + round_up(pairs * (size_t)scan_splits(B, Hkv, Lcap) * sizeof(int), kAlign);
@@ -206,6 +243,21 @@ void launch_scan(int bits, int nt, int mode, dim3 grid, hipStream_t stream, cons
     else launch_scan_bits<8>(nt, mode, grid, stream, sa);
 }
 
+// The fused top-delta kernel for this depth, head tiling and pseudo-max source.
+template <int NT, int BITS>
+void launch_fused_nt(int mode, dim3 grid, hipStream_t stream, const FusedArgs& fa) {
+    if (mode == kSelRefinedPM)
+        hipLaunchKernelGGL((ffd_decode_kernel<NT, BITS, kSelRefinedPM>), grid, dim3(kScanThreads), 0, stream, fa);
+    else
+        hipLaunchKernelGGL((ffd_decode_kernel<NT, BITS, kSelThumbnailPM>), grid, dim3(kScanThreads), 0, stream, fa);
+}
+
+void launch_fused(int bits, int nt, int mode, dim3 grid, hipStream_t stream, const FusedArgs& fa) {
+    if (bits == 2) nt == 1 ? launch_fused_nt<1, 2>(mode, grid, stream, fa) : launch_fused_nt<2, 2>(mode, grid, stream, fa);
+    else if (bits == 4) nt == 1 ? launch_fused_nt<1, 4>(mode, grid, stream, fa) : launch_fused_nt<2, 4>(mode, grid, stream, fa);
+    else nt == 1 ? launch_fused_nt<1, 8>(mode, grid, stream, fa) : launch_fused_nt<2, 8>(mode, grid, stream, fa);
+}
+
 // The refinement kernel, recomputing the scan scores from rbits-bit codes.
 template <int NT>
 void launch_refine_nt(int rbits, dim3 grid, hipStream_t stream, const RefineArgs& ra) {
@@ -225,8 +277,12 @@ int decode_checks(const void* q, const void* k_codes, const void* k_absmax, cons
     const float* m_tilde = extras ? extras->m_tilde : nullptr;
     const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
     const int top_k = extras ? extras->top_k : 0;
+    const int kernels = extras ? extras->kernels : FFD_KERNELS_AUTO;
     if (pm_source != FFD_PSEUDO_MAX_THUMBNAIL && pm_source != FFD_PSEUDO_MAX_REFINED)
         return FFD_ERR_INVALID_ARGUMENT;
+    if (kernels != FFD_KERNELS_AUTO && kernels != FFD_KERNELS_FUSED && kernels != FFD_KERNELS_SPLIT)
+        return FFD_ERR_INVALID_ARGUMENT;
+    if (top_k > 0 && kernels == FFD_KERNELS_FUSED) return FFD_ERR_INVALID_ARGUMENT;
     if (top_k < 0 || (top_k > 0 && m_tilde)) return FFD_ERR_INVALID_ARGUMENT;
     if (block_size != FFD_BLOCK) return block_size > 0 ? FFD_ERR_UNSUPPORTED : FFD_ERR_INVALID_ARGUMENT;
     if (std::isnan(delta) || delta < 0.f || n_sink < 0 || n_local < 0) return FFD_ERR_INVALID_ARGUMENT;
@@ -251,6 +307,16 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
     return resolve_splits(B, Hkv, Lcap, num_splits);
 }
 
+int ffd_fused_splits(int B, int Hkv, int Lcap, int num_splits) {
+    return decode_splits(B, Hkv, Lcap, num_splits);
+}
+
+int ffd_select_kernels(int B, int Hkv, int Lcap, int num_splits) {
+    const int S1f = decode_splits(B, Hkv, Lcap, num_splits);
+    if (S1f <= 0) return 0;
+    return auto_kernels(Lcap, S1f);
+}
+
 int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
     return resolve_splits(B, Hkv, Lcap, num_splits, true);
 }
@@ -265,10 +331,12 @@ size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int nu
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
     const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
-    if (S <= 0) return 0;
+    const int S1f = decode_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits);
+    if (S <= 0 || S1f <= 0) return 0;
     if ((long long)B * Hkv > (1LL << 20) || Lcap / FFD_BLOCK > kFfdMaxScanBlocks * kFfdMaxScanSplits) return 0;
     // enough for the dense entry point with the same num_splits too
-    return std::max(ffd_layout(B, Hq, Hkv, Lcap, D, S).total, ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits));
+    return std::max(ffd_layout(B, Hq, Hkv, Lcap, D, S, S1f).total,
+                    ffd_dense_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits));
 }
 
 const char* ffd_status_string(int status) {
@@ -340,6 +408,7 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     float* m_tilde = extras ? extras->m_tilde : nullptr;
     const int pm_source = extras ? extras->pseudo_max : FFD_PSEUDO_MAX_THUMBNAIL;
     const int top_k = extras ? extras->top_k : 0;
+    const int kernels_req = extras ? extras->kernels : FFD_KERNELS_AUTO;
     int S = 0;
     int st = decode_checks(q, k_codes, k_absmax, k_resid, v, seq_lens, B, Hq, Hkv, Lcap, D, thumb_bits,
                            block_size, delta, n_sink, n_local, num_splits, softmax_scale, out, lse,
@@ -348,7 +417,8 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
     if (workspace_bytes < ffd_workspace_bytes(B, Hq, Hkv, Lcap, D, num_splits)) return FFD_ERR_WORKSPACE_TOO_SMALL;
     const int G = Hq / Hkv;
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
-    const FfdWorkspace W = ffd_layout(B, Hq, Hkv, Lcap, D, S);
+    const int S1f = decode_splits(B, Hkv, Lcap, num_splits);
+    const FfdWorkspace W = ffd_layout(B, Hq, Hkv, Lcap, D, S, S1f);
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     float* part_m = reinterpret_cast<float*>(ws);
     float* part_l = part_m + W.rows;
@@ -377,6 +447,25 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
 
     const int mode = top_k > 0 ? kSelTopK : (pm_source == FFD_PSEUDO_MAX_REFINED ? kSelRefinedPM : kSelThumbnailPM);
     if ((st = mark(0)) != FFD_OK) return st;
+    const int kernels = kernels_req == FFD_KERNELS_AUTO ? auto_kernels(Lcap, S1f) : kernels_req;
+    if (top_k == 0 && kernels == FFD_KERNELS_FUSED) {
+        // top-delta, fused: one kernel, then the merge of its S1f partial states per head (none when
+        // S1f == 1: the kernel writes the outputs itself)
+        const bool direct = S1f == 1;
+        FusedArgs fa{static_cast<const uint16_t*>(q), static_cast<const uint32_t*>(k_codes),
+                     static_cast<const uint16_t*>(k_absmax), static_cast<const int8_t*>(k_resid),
+                     static_cast<const uint16_t*>(v), seq_lens, block_mask, m_tilde, part_m, part_l, part_acc,
+                     direct ? static_cast<uint16_t*>(out) : nullptr, direct ? lse : nullptr,
+                     Hq, Hkv, Lcap, G, S1f, delta, scale, n_sink, n_local};
+        launch_fused(thumb_bits, G <= 4 ? 1 : 2, mode, dim3((unsigned)S1f, (unsigned)Hkv, (unsigned)B), stream, fa);
+        if ((st = launch_status()) != FFD_OK || (st = mark(1)) != FFD_OK || (st = mark(2)) != FFD_OK) return st;
+        if (!direct) {
+            hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, part_m,
+                               part_l, part_acc, S1f, nullptr, 1, static_cast<uint16_t*>(out), lse);
+            if ((st = launch_status()) != FFD_OK) return st;
+        }
+        return mark(3);
+    }
     launch_scan(thumb_bits, G <= 4 ? 1 : 2, mode, scan_grid, stream, sa);
     if ((st = launch_status()) != FFD_OK) return st;
     if (top_k > 0) {

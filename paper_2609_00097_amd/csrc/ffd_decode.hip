@@ -631,6 +631,276 @@ __global__ __launch_bounds__(kScanThreads, scan_occupancy<BITS>()) void ffd_scan
 }
 
 // ================================================================================================
+// Fused top-delta decode: one workgroup per (sequence, KV head, split s) of kScanWaves waves.
+// Workgroup s owns the blocks j = s + S1 i (i < cnt) of its group, an interleaved share, so the kept
+// blocks of a group (windows, planted clusters) spread evenly over its S1 workgroups. It
+//  1. streams the thumbnail codes of its blocks (waves take block numbers i from an LDS counter,
+//     kRing blocks in flight each) and keeps each block's per-head maximum score in LDS, while each
+//     wave also scores its share of the pseudo-max window blocks (Alg. 1; Eq. 3);
+//  2. decides per (head, block): keep iff sigma >= m~ - delta (Eq. 1), the kept blocks (with their
+//     keep bits) forming a list in LDS, in block order;
+//  3. refines and attends its own kept blocks (Eq. 4; online softmax and PV): wave w takes tile
+//     w % 4 of the kept entries w / 4, w / 4 + 2, ..., with kRefineRing tiles in flight; the
+//     thumbnail term of each kept tile is recomputed from its codes with the same integer MFMA and
+//     fp32 operations as in step 1, so it equals the value the decision used;
+//  4. combines the eight waves' states into one partial state per head (rows [B, Hq, S1]), or,
+//     when it is the group's only workgroup (S1 == 1), writes the bf16 output and lse itself.
+// No workgroup waits for another: each needs only its own blocks, the window blocks (re-read by
+// every workgroup of the group, L2-resident) and the query.
+// ================================================================================================
+template <int NT>
+struct FusedLds {
+    QueryLds<NT> qs;
+    alignas(16) float pm[kScanWaves][4 * NT];             // each wave's window maxima per head
+    alignas(16) float sig[kFfdMaxScanBlocks][4 * NT];     // block maxima per head, by share index i
+    uint32_t list[kFfdMaxScanBlocks];                     // kept blocks j | keep bits << 24
+    int nkept[kScanWaves];
+    int next;                                             // next share index to hand out
+    TileP<NT> tp[kScanWaves];
+    EpilogueLds<NT, kScanWaves> epi;
+};
+
+template <int NT, int BITS, int MODE>
+__global__ __launch_bounds__(kScanThreads, 1) void ffd_decode_kernel(FusedArgs a) {
+    static_assert(MODE == kSelThumbnailPM || MODE == kSelRefinedPM, "top-delta modes only");
+    constexpr int kRing = scan_ring<BITS>();
+    __shared__ FusedLds<NT> sm;
+    const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 4, n = lane & 15;
+    const int G = a.G, hq0 = kvh * G, S1 = a.S1;
+    const size_t bh = (size_t)b * a.Hkv + kvh;
+    const size_t hrow0 = (size_t)b * a.Hq + hq0;             // [B, Hq] row of the group's head 0
+    const int L = min(max(a.seq_lens[b], 0), a.Lcap);
+    const int nblk = (L + kBlock - 1) / kBlock;
+    const int nblk_cap = a.Lcap / kBlock;
+    const int cnt = nblk > s ? (nblk - 1 - s) / S1 + 1 : 0;  // blocks of this workgroup
+    uint16_t* out_h = a.out ? a.out + hrow0 * kD : nullptr;
+    float* lse_h = a.out && a.lse ? a.lse + hrow0 : nullptr;
+
+    // Mask entries past the end of the sequence are zero (spread over the group's workgroups).
+    if (a.mask) {
+        for (int j = nblk + s * kScanThreads + tid; j < nblk_cap; j += S1 * kScanThreads)
+            for (int h = 0; h < G; ++h) a.mask[(hrow0 + h) * nblk_cap + j] = 0;
+    }
+    if (cnt == 0) {                                 // uniform: nothing to scan
+        if (out_h) {                                // an empty sequence: out = 0, lse = -inf
+            for (int idx = tid; idx < G * kD; idx += kScanThreads) out_h[idx] = 0;
+            if (lse_h && tid < G) lse_h[tid] = -INFINITY;
+        } else if (tid < G) {
+            a.part_m[(hrow0 + tid) * S1 + s] = -INFINITY;     // an empty partial state
+        }
+        if (a.m_tilde && s == 0 && tid < G) a.m_tilde[hrow0 + tid] = -INFINITY;   // L = 0
+        return;
+    }
+
+    const uint32_t* codes_bh = a.codes + bh * (size_t)a.Lcap * (4 * BITS);
+    const uint16_t* absmax_bh = a.absmax + bh * (size_t)a.Lcap;
+
+    // The stream reads through buffer resources whose ranges end after this workgroup's last block
+    // s + S1 (cnt - 1): a request for an index i >= cnt (block s + S1 i beyond it) reads zeros
+    // without touching memory, so every load is issued unconditionally (uniform control flow keeps
+    // the compiler's in-order vmcnt accounting exact). Offsets are unsigned 32-bit: at most 2^18 + S1
+    // blocks of 8 KiB.
+    const uint32_t jend = (uint32_t)(s + S1 * (cnt - 1)) + 1u;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(codes_bh), (short)0, (int)(jend * (1024u * BITS)), kRawBufferWord3);
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(absmax_bh), (short)0, (int)(jend * 128u), kRawBufferWord3);
+    auto block_of = [&](int i) { return s + S1 * min(i, cnt); };     // i >= cnt: past the range
+    int is[kRing];                                  // share index held by each ring slot (>= cnt: none)
+#pragma unroll
+    for (int r = 0; r < kRing; ++r) is[r] = kRing * wave + r;
+
+    // Requests: queries, the first window blocks, the first ring round.
+    uint32_t qw[NT];
+    load_query_words<NT>(a.q, b, a.Hq, hq0, G, wave, lane, qw);
+    const int jlast = nblk - 1;
+    const int sink_end = min(a.n_sink, L);
+    const int loc_beg = max(0, L - a.n_local);
+    const int sink_blk_end = (sink_end + kBlock - 1) / kBlock;
+    const int loc_blk_beg = max(loc_beg / kBlock, sink_blk_end);
+    const int npm = sink_blk_end + max(nblk - loc_blk_beg, 0);
+    auto pm_block = [&](int idx) { return idx < sink_blk_end ? idx : loc_blk_beg + (idx - sink_blk_end); };
+    auto win_block = [&](int idx) { return min(pm_block(min(idx, max(npm, 1) - 1)), jlast); };
+    constexpr bool kEarlyWindows = MODE == kSelThumbnailPM;
+    BlockScan<BITS> win;
+    auto load_window = [&](int base) { win = load_block_scan<BITS>(codes_bh, absmax_bh, win_block(base + wave), lane); };
+    if constexpr (kEarlyWindows) load_window(0);
+    BlockScan<BITS> ring[kRing];
+#pragma unroll
+    for (int r = 0; r < kRing; ++r) ring[r] = load_block_scan_rsrc<BITS>(rc, ra, block_of(is[r]), lane);
+    if (tid == 0) sm.next = kScanWaves * kRing;
+    if constexpr (MODE == kSelRefinedPM) load_window(0);
+
+    HeadConsts<NT> hc;
+    build_query_consts<NT>(sm.qs, qw, G, a.scale, thumb_top_level(BITS), tid, hc);
+
+    // ---- scan (Alg. 1): block maxima per head, and the window maxima of the pseudo-max ---------
+    float pm[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) pm[t] = -INFINITY;
+    auto window_pass = [&](int base) {
+        const int idx = base + wave;
+        if (idx >= npm) return;                     // wave-uniform
+        const int j = pm_block(idx);
+        float sc[NT][4];
+        block_scores<NT, BITS>(win, j, lane, L, hc, sc);
+        if constexpr (MODE == kSelRefinedPM)
+            add_residual_term<NT>(a.resid + bh * (size_t)a.Lcap * kD, win.mm, j, lane, hc, sc);
+#pragma unroll
+        for (int T4 = 0; T4 < 4; ++T4) {
+            const int tok = 64 * j + 16 * T4 + n;
+            const bool in_win = tok < L && (tok < sink_end || tok >= loc_beg);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) pm[t] = fmaxf(pm[t], in_win ? sc[t][T4] : -INFINITY);
+        }
+    };
+    auto consume = [&](const BlockScan<BITS>& blk, int i) {
+        float sc[NT][4];
+        block_scores<NT, BITS>(blk, s + S1 * i, lane, L, hc, sc);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float sig = row16_max(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3])));
+            if (n == 0) sm.sig[i][4 * t + g] = sig;
+        }
+    };
+    if constexpr (kEarlyWindows) window_pass(0);
+    for (bool more = true; more;) {                 // wave-uniform
+        more = false;
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+            int in = 0;
+            if (lane == 0) in = atomicAdd(&sm.next, 1);
+            in = __builtin_amdgcn_readfirstlane(in);
+            if (is[r] < cnt) consume(ring[r], is[r]);
+            ring[r] = load_block_scan_rsrc<BITS>(rc, ra, block_of(in), lane);
+            is[r] = in;
+            more |= in < cnt;
+        }
+    }
+    if constexpr (!kEarlyWindows) window_pass(0);
+    for (int base = kScanWaves; base < npm; base += kScanWaves) {
+        load_window(base);
+        window_pass(base);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        pm[t] = row16_max(pm[t]);
+        if (n == 0) sm.pm[wave][4 * t + g] = pm[t];
+    }
+    __syncthreads();
+
+    // ---- decide (Eq. 1): keep iff sigma >= m~ - delta; the kept list in LDS, in block order ----
+    float thr[4 * NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        float4 m = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+#pragma unroll
+        for (int w = 0; w < kScanWaves; ++w) {
+            const float4 p = reinterpret_cast<const float4*>(sm.pm[w])[t];
+            m.x = fmaxf(m.x, p.x); m.y = fmaxf(m.y, p.y); m.z = fmaxf(m.z, p.z); m.w = fmaxf(m.w, p.w);
+        }
+        thr[4 * t] = m.x - a.delta;                 // -inf when both windows are empty
+        thr[4 * t + 1] = m.y - a.delta;
+        thr[4 * t + 2] = m.z - a.delta;
+        thr[4 * t + 3] = m.w - a.delta;
+    }
+    if (a.m_tilde && s == 0 && tid < G) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kScanWaves; ++w) m = fmaxf(m, sm.pm[w][tid]);
+        a.m_tilde[hrow0 + tid] = m;
+    }
+    // lane l of wave w decides share index 64 w + l (cnt <= kFfdMaxScanBlocks <= 64 kScanWaves)
+    static_assert(kFfdMaxScanBlocks <= 64 * kScanWaves, "one decision per lane");
+    uint32_t bits = 0;
+    const int il = 64 * wave + lane;
+    const int jl = s + S1 * il;
+    if (il < cnt) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float4 sg = reinterpret_cast<const float4*>(sm.sig[il])[t];
+            bits |= ((uint32_t)(sg.x >= thr[4 * t]) | (uint32_t)(sg.y >= thr[4 * t + 1]) << 1 |
+                     (uint32_t)(sg.z >= thr[4 * t + 2]) << 2 | (uint32_t)(sg.w >= thr[4 * t + 3]) << 3) << (4 * t);
+        }
+        bits &= (1u << G) - 1u;                     // heads past G are never kept
+        if (a.mask)
+            for (int h = 0; h < G; ++h) a.mask[(hrow0 + h) * nblk_cap + jl] = (bits >> h) & 1u;
+    }
+    const uint64_t kept = __ballot(bits != 0);
+    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(kept >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)kept, 0u));
+    if (lane == 0) sm.nkept[wave] = __popcll(kept);
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kScanWaves; ++w) {
+        const int c = sm.nkept[w];
+        before += w < wave ? c : 0;
+        total += c;
+    }
+    if (bits != 0) sm.list[before + below] = (uint32_t)jl | (bits << 24);
+    __syncthreads();
+
+    // ---- refine (Eq. 4) and attend the kept blocks: wave w, tile T4 = w % 4, entries w / 4 + 2k --
+    const int T4 = wave & 3, par = wave >> 2;
+    const int mine = total > par ? (total - par + 1) / 2 : 0;
+    const int8_t* resid_bh = a.resid + bh * (size_t)a.Lcap * kD;
+    const uint16_t* v_bh = a.v + bh * (size_t)a.Lcap * kD;
+    PvAcc<NT> pv;
+    pv.zero();
+    float m_run[NT], l_part[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) { m_run[t] = -INFINITY; l_part[t] = 0.f; }
+    TileP<NT>& tp = sm.tp[wave];
+    auto entry = [&](int k) { return sm.list[par + 2 * min(k, mine - 1)]; };
+    auto attend = [&](const RefineTile<NT, BITS>& rt, int j, uint32_t kb) {
+        float z[NT];
+        bool keep[NT];
+        const float Mt = bf16_to_f32((uint16_t)rt.m);
+        float shat[NT];                             // Eq. 4's first term: the scan scores, recomputed
+        tile_scores<NT, BITS>(rt.cw, Mt, 64 * j + 16 * T4 + n < L, hc, shat);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            v4i acc = {0, 0, 0, 0};
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][0], rt.r0, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(hc.A[t][1], rt.r1, acc, 0, 0, 0);
+            const float R = fmaf(65536.f, (float)acc.z, fmaf(256.f, (float)acc.y, (float)acc.x));
+            const float sct = shat[t];
+            z[t] = sct == -INFINITY ? -INFINITY : fmaf(R, Mt * hc.kap2[t], sct);
+            keep[t] = (kb >> (4 * t + g)) & 1u;
+        }
+        softmax_tile<NT>(z, keep, m_run, l_part, tp, g, n);
+        wave_lds_fence();
+        pv_tile<NT>(pv, tp, rt.vt);
+        wave_lds_fence();
+    };
+    if (mine > 0) {                                 // wave-uniform
+        RefineTile<NT, BITS> rr[kRefineRing];
+#pragma unroll
+        for (int r = 0; r < kRefineRing; ++r)
+            rr[r] = load_refine_tile<NT, BITS>(resid_bh, v_bh, codes_bh, absmax_bh,
+                                               (int)(entry(r) & 0xffffffu), T4, lane, L);
+        for (int k0 = 0; k0 < mine; k0 += kRefineRing) {
+#pragma unroll
+            for (int r = 0; r < kRefineRing; ++r) {
+                const int k = k0 + r;
+                if (k < mine) {
+                    const uint32_t e = entry(k);
+                    attend(rr[r], (int)(e & 0xffffffu), e >> 24);
+                }
+                // the last round's refills re-read the wave's last tile (clamped): still cached
+                rr[r] = load_refine_tile<NT, BITS>(resid_bh, v_bh, codes_bh, absmax_bh,
+                                                   (int)(entry(k + kRefineRing) & 0xffffffu), T4, lane, L);
+            }
+        }
+    }
+
+    write_partials<NT, kScanWaves>(sm.epi, pv, m_run, l_part, wave, lane, G, hrow0 * S1 + s, (size_t)S1,
+                                   a.part_m, a.part_l, a.part_acc, out_h, lse_h);
+}
+
+// ================================================================================================
 // Refinement: Eq. 4 on the kept blocks, online softmax and PV, one partial state per workgroup.
 // Grid (W + B*Hkv). With N kept blocks in all and n_x in KV group x, group x gets
 // W_x = ceil(n_x * min(W, N) / N) workgroups (1 if n_x = 0) in group order; workgroup p of the
@@ -980,6 +1250,18 @@ template __global__ void ffd_scan_kernel<1, 4, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<2, 4, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<1, 8, kSelTopK>(ScanArgs);
 template __global__ void ffd_scan_kernel<2, 8, kSelTopK>(ScanArgs);
+template __global__ void ffd_decode_kernel<1, 2, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 2, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<1, 4, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 4, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<1, 8, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 8, kSelThumbnailPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<1, 2, kSelRefinedPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 2, kSelRefinedPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<1, 4, kSelRefinedPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 4, kSelRefinedPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<1, 8, kSelRefinedPM>(FusedArgs);
+template __global__ void ffd_decode_kernel<2, 8, kSelRefinedPM>(FusedArgs);
 template __global__ void ffd_refine_kernel<1, 2>(RefineArgs);
 template __global__ void ffd_refine_kernel<2, 2>(RefineArgs);
 template __global__ void ffd_refine_kernel<1, 4>(RefineArgs);

@@ -219,20 +219,24 @@ __device__ __forceinline__ void softmax_tile(const float (&z)[NT], const bool (&
     }
 }
 
-// Workgroup epilogue: combine the four waves' (m, l, acc) and write one partial state per head.
-// Head h (0 <= h < G) of the group goes to partial row row0 + h * head_stride.
-template <int NT>
+// Workgroup epilogue: combine the NW waves' (m, l, acc) and write one partial state per head.
+// Head h (0 <= h < G) of the group goes to partial row row0 + h * head_stride. With out != null the
+// workgroup holds the head's only partial state, so it writes the normalised bf16 output row
+// out + h * kD and lse[h] (when lse != null) instead, as lse_merge_kernel would from that one row:
+// out = acc / l, lse = m + ln l; no kept token gives out = 0 and lse = -inf.
+template <int NT, int NW = kWaves>
 struct EpilogueLds {
-    float m[kWaves][4 * NT];
-    float l[kWaves][4 * NT];
-    float acc[kWaves][4 * NT][kD];
+    float m[NW][4 * NT];
+    float l[NW][4 * NT];
+    float acc[NW][4 * NT][kD];
 };
 
-template <int NT>
-__device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<NT>& pv,
+template <int NT, int NW = kWaves>
+__device__ __forceinline__ void write_partials(EpilogueLds<NT, NW>& E, const PvAcc<NT>& pv,
                                                const float (&m_run)[NT], const float (&l_part)[NT],
                                                int wave, int lane, int G, size_t row0, size_t head_stride,
-                                               float* part_m, float* part_l, float* part_acc) {
+                                               float* part_m, float* part_l, float* part_acc,
+                                               uint16_t* out = nullptr, float* lse = nullptr) {
     const int g = lane >> 4, n = lane & 15;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -246,15 +250,15 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
     for (int h = 0; h < 4 * NT; ++h)
         *reinterpret_cast<float2*>(&E.acc[wave][h][2 * lane]) = make_float2(pv.acc[h][0], pv.acc[h][1]);
     __syncthreads();
-    for (int idx = threadIdx.x; idx < G * kD; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < G * kD; idx += 64 * NW) {
         const int h = idx >> 7, d = idx & (kD - 1);
         float mx = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, E.m[w][h]);
+        for (int w = 0; w < NW; ++w) mx = fmaxf(mx, E.m[w][h]);
         float l = 0.f, a = 0.f;
         if (mx != -INFINITY) {
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) {
+            for (int w = 0; w < NW; ++w) {
                 const float mw = E.m[w][h];
                 if (mw != -INFINITY) {
                     const float sc = __expf(mw - mx);
@@ -262,6 +266,12 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
                     a = fmaf(sc, E.acc[w][h][d], a);
                 }
             }
+        }
+        if (out) {
+            const bool any = mx != -INFINITY;
+            out[(size_t)h * kD + d] = f32_to_bf16(a * (any ? 1.f / l : 0.f));
+            if (lse && d == 0) lse[h] = any ? mx + logf(l) : -INFINITY;
+            continue;
         }
         const size_t row = row0 + (size_t)h * head_stride;
         part_acc[row * kD + d] = a;
@@ -274,15 +284,15 @@ __device__ __forceinline__ void write_partials(EpilogueLds<NT>& E, const PvAcc<N
 
 // Log-sum-exp merge of `count` partial rows row0 + i * stride (i < count) of one head into its bf16
 // output row and lse (Sec. 2, flash-decoding): M* = max m_i, l* = sum e^{m_i - M*} l_i,
-// out = sum e^{m_i - M*} acc_i / l*, lse = M* + ln l*. Rows with m = -inf are skipped; no row
-// gives out = 0, lse = -inf. Run by all 256 threads of a workgroup: thread (d4, r) folds rows
+// out = sum e^{m_i - M*} acc_i / l*, lse = M* + ln l*. Rows with m = -inf are skipped (their l and
+// acc may hold anything); no row gives out = 0, lse = -inf. Run by all 256 threads of a workgroup: thread (d4, r) folds rows
 // i = r (mod 8) of dims 4*d4 .. 4*d4 + 3, U rows at a time with the next U rows' loads already in
 // flight (a head can have hundreds of partials), then the 8 threads of a d4 combine with shuffles.
 constexpr int kMergeLanes = 8;
 
 __device__ __forceinline__ void lse_fold(float& M, float& l, float4& acc, float m2, float l2, float4 a2) {
+    if (m2 == -INFINITY) return;               // an empty row: its l and acc are not read
     const float mn = fmaxf(M, m2);
-    if (mn == -INFINITY) return;
     const float c1 = __expf(M - mn), c2 = __expf(m2 - mn);
     l = l * c1 + l2 * c2;
     acc.x = acc.x * c1 + a2.x * c2;

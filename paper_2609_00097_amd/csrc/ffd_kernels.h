@@ -53,6 +53,27 @@ struct RefineArgs {
     float top_level;            // Lv of the thumbnail depth: the residual step is M / (254 Lv)
 };
 
+// The fused top-delta decode kernel: scan, pseudo-max, decisions, refinement and attention in one
+// workgroup per (sequence, KV head, split), on an interleaved share of the group's blocks.
+struct FusedArgs {
+    const uint16_t* q;          // bf16 [B, Hq, 128]
+    const uint32_t* codes;      // [B, Hkv, Lcap/64, 64, 4b]
+    const uint16_t* absmax;     // bf16 [B, Hkv, Lcap/64, 16, 4]
+    const int8_t* resid;        // [B, Hkv, Lcap/16, 2, 64, 16]
+    const uint16_t* v;          // bf16 [B, Hkv, Lcap, 128]
+    const int32_t* seq_lens;    // [B]
+    uint8_t* mask;              // [B, Hq, Lcap/64] or null
+    float* m_tilde;             // [B, Hq] or null: the pseudo-max of each head
+    float* part_m;              // [B, Hq, S1] partial states (S1 > 1)
+    float* part_l;
+    float* part_acc;            // [B, Hq, S1, 128]
+    uint16_t* out;              // bf16 [B, Hq, 128], written by the kernel itself when S1 == 1, else null
+    float* lse;                 // [B, Hq] or null (S1 == 1 only)
+    int Hq, Hkv, Lcap, G, S1;
+    float delta, scale;
+    int n_sink, n_local;
+};
+
 // Fixed-budget (top-k) selection over the block scores the scan kernel wrote; its output takes the
 // place of the scan's kept lists and counts (each group's whole list in split 0).
 struct TopkArgs {
@@ -103,6 +124,9 @@ struct AppendArgs {
 // The first two write the kept lists and counts; no mode stores the scan scores.
 enum ScanMode { kSelThumbnailPM = 0, kSelRefinedPM = 1, kSelTopK = 2 };
 template <int NT, int BITS, int MODE> __global__ void ffd_scan_kernel(ScanArgs a);
+// MODE kSelThumbnailPM or kSelRefinedPM; the scan scores of the kept tiles are recomputed from the
+// codes the kernel has just streamed (bit for bit the values the decisions used).
+template <int NT, int BITS, int MODE> __global__ void ffd_decode_kernel(FusedArgs a);
 // The scan scores of the kept tiles (Eq. 4's first term) are recomputed from the RBITS-bit codes with
 // the scan kernel's own integer MFMA and fp32 operations, so they equal the scan's bit for bit.
 template <int NT, int RBITS> __global__ void ffd_refine_kernel(RefineArgs a);

@@ -25,7 +25,8 @@ NOALLOC_SCRATCH_BYTES = 16 << 20     # FFD_NOALLOC_SCRATCH_BYTES
 
 EXPORTS = ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
            "ffd_decode_attention_noalloc", "ffd_dense_decode_attention",
-           "ffd_resolve_splits", "ffd_dense_resolve_splits", "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
+           "ffd_resolve_splits", "ffd_fused_splits", "ffd_select_kernels", "ffd_dense_resolve_splits",
+           "ffd_workspace_bytes", "ffd_dense_workspace_bytes", "ffd_status_string")
 
 
 class FfdLibraryError(RuntimeError):
@@ -45,10 +46,13 @@ P, I, F, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 PSEUDO_MAX = {"thumbnail": 0, "refined": 1}     # FFD_PSEUDO_MAX_THUMBNAIL, FFD_PSEUDO_MAX_REFINED
 
 
+KERNELS = {"auto": 0, "fused": 1, "split": 2}     # FFD_KERNELS_AUTO, _FUSED, _SPLIT
+
+
 class DecodeExtras(ctypes.Structure):
-    """``ffd_decode_extras``: stage events, the pseudo-max output, the pseudo-max source and the
-    fixed-budget (top-k) selection."""
-    _fields_ = [("stage_events", P), ("m_tilde", P), ("pseudo_max", I), ("top_k", I)]
+    """``ffd_decode_extras``: stage events, the pseudo-max output, the pseudo-max source, the
+    fixed-budget (top-k) selection and the top-delta kernels."""
+    _fields_ = [("stage_events", P), ("m_tilde", P), ("pseudo_max", I), ("top_k", I), ("kernels", I)]
 
 
 def lib() -> ctypes.CDLL:
@@ -71,6 +75,8 @@ def lib() -> ctypes.CDLL:
                                                 P, P, P, P]
     so.ffd_dense_decode_attention.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P, P, P, SZ, P]
     so.ffd_resolve_splits.argtypes = [I, I, I, I]
+    so.ffd_fused_splits.argtypes = [I, I, I, I]
+    so.ffd_select_kernels.argtypes = [I, I, I, I]
     so.ffd_dense_resolve_splits.argtypes = [I, I, I, I]
     for name in ("ffd_workspace_bytes", "ffd_dense_workspace_bytes"):
         getattr(so, name).argtypes = [I, I, I, I, I, I]
@@ -79,7 +85,7 @@ def lib() -> ctypes.CDLL:
     so.ffd_status_string.restype = ctypes.c_char_p
     for name in ("ffd_quantize_keys", "ffd_append_kv", "ffd_decode_attention", "ffd_decode_attention_ex",
                  "ffd_decode_attention_noalloc", "ffd_dense_decode_attention", "ffd_resolve_splits",
-                 "ffd_dense_resolve_splits"):
+                 "ffd_fused_splits", "ffd_select_kernels", "ffd_dense_resolve_splits"):
         getattr(so, name).restype = I
     _lib = so
     return so
@@ -110,8 +116,20 @@ def _need(t, name, dtype, shape=None):
 
 
 def resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
-    """Splits an FFD call with this ``num_splits`` uses (0 = automatic)."""
+    """Refinement workgroups per KV group (on average) of the split kernels for this ``num_splits``
+    (0 = automatic)."""
     return lib().ffd_resolve_splits(B, Hkv, Lcap, num_splits)
+
+
+def fused_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
+    """Workgroups per KV group of the fused top-delta kernel for this ``num_splits``."""
+    return lib().ffd_fused_splits(B, Hkv, Lcap, num_splits)
+
+
+def select_kernels(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> str:
+    """The top-delta kernels the automatic choice uses: ``"fused"`` or ``"split"``."""
+    k = lib().ffd_select_kernels(B, Hkv, Lcap, num_splits)
+    return {1: "fused", 2: "split"}[k]
 
 
 def dense_resolve_splits(B: int, Hkv: int, Lcap: int, num_splits: int = 0) -> int:
@@ -220,7 +238,7 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
                      n_local: int = 256, num_splits: int = 0, softmax_scale: float = 0.0,
                      return_lse: bool = True, return_mask: bool = False, workspace=None,
                      out=None, lse=None, mask=None, stage_events=None, m_tilde=None,
-                     pseudo_max: str = "thumbnail", top_k: int = 0):
+                     pseudo_max: str = "thumbnail", top_k: int = 0, kernels: str = "auto"):
     """FFD decode attention. Returns ``(out, lse, mask)`` (lse/mask None unless requested).
     The thumbnail depth is that of ``codes`` (its last dimension is 4 words per bit).
 
@@ -230,7 +248,8 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
     pseudo-max. ``pseudo_max``: ``"thumbnail"`` (default) or ``"refined"``, the scores of the window
     tokens the pseudo-max is taken over. ``top_k > 0`` replaces the top-delta rule by the fixed
     budget of ``top_k`` blocks per head (largest thumbnail block scores, ties in block order); delta
-    and the windows are then unused and ``m_tilde`` must be None."""
+    and the windows are then unused and ``m_tilde`` must be None. ``kernels``: ``"auto"``,
+    ``"fused"`` or ``"split"`` (top-delta's kernels; see ``FFD_KERNELS_*`` in ffd.h)."""
     B, Hq, D = q.shape
     Hkv, Lcap = v.shape[1], v.shape[2]
     _need(q, "q", torch.bfloat16)
@@ -250,8 +269,10 @@ def decode_attention(q, codes, absmax, resid, v, seq_lens, *, delta: float, n_si
         if len(stage_events) != 4 or any(e.cuda_event == 0 for e in stage_events):
             raise ValueError("stage_events must be four recorded torch.cuda.Event objects")
         ev = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
+    if kernels not in KERNELS:
+        raise ValueError(f"kernels must be one of {tuple(KERNELS)}")
     extras = DecodeExtras(ctypes.cast(ev, P) if ev is not None else None, _ptr(m_tilde),
-                          PSEUDO_MAX[pseudo_max], int(top_k))
+                          PSEUDO_MAX[pseudo_max], int(top_k), KERNELS[kernels])
     _check("ffd_decode_attention", lib().ffd_decode_attention_ex(
         _ptr(q), _ptr(codes), _ptr(absmax), _ptr(resid), _ptr(v), _ptr(seq_lens), B, Hq, Hkv, Lcap,
         D, bits, BLOCK, float(delta), n_sink, n_local, num_splits, float(softmax_scale), _ptr(out),

@@ -43,20 +43,40 @@ def test_status_strings(so):
 
 
 def test_splits_and_workspace_sizes(so):
+    # split kernels: (S + 1) * B * Hkv refinement workgroups, one per CU (no GPU here: 256 CUs)
     assert so.ffd_resolve_splits(4, 8, 131072, 0) == 7            # (7 + 1) * 32 = 256 refinement workgroups
     assert so.ffd_resolve_splits(1, 2, 4096, 0) == 8              # capped: 64 blocks / 8 per split
     assert so.ffd_resolve_splits(4, 6, 131072, 0) == 9            # (9 + 1) * 24 = 240 <= 256
     assert so.ffd_resolve_splits(64, 8, 131072, 0) == 1           # at least one split
-    assert so.ffd_dense_resolve_splits(4, 8, 131072, 0) == 15     # dense: 512 workgroups
-    assert so.ffd_dense_resolve_splits(4, 8, 131072, 5) == 5
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
-    # partials (S*P + P)*G*(D+2)*4 | table P*8 | counts P*S1*4 | lists P*C*4 | block scores P*C*G*4,
-    # each region on a 256-byte boundary (S1 = 8 scan splits at 4 x 8 x 128K, 4 at 1 x 2 x 4K)
+    # fused kernel: S1 workgroups per (sequence, KV head), about one per CU in all (floor), each with
+    # >= 64 blocks of the capacity, never fewer than blocks / 256
+    assert so.ffd_fused_splits(4, 8, 131072, 0) == 8              # 32 groups x 8 = 256 workgroups
+    assert so.ffd_fused_splits(1, 2, 4096, 0) == 1                # 64 blocks: one workgroup, no merge
+    assert so.ffd_fused_splits(1, 8, 32768, 0) == 8               # capped: 512 blocks / 64
+    assert so.ffd_fused_splits(4, 6, 131072, 0) == 10             # floor(256 / 24)
+    assert so.ffd_fused_splits(64, 8, 131072, 0) == 8             # at least 2048 / 256
+    assert so.ffd_fused_splits(4, 8, 131072, 7) == 8              # raised to 2048 / 256
+    assert so.ffd_fused_splits(4, 8, 131072, 12) == 12
+    assert so.ffd_fused_splits(4, 8, 131072, 5000) == 0
+    # automatic kernels: fused while a workgroup covers at most 64 blocks (1 = fused, 2 = split)
+    assert so.ffd_select_kernels(1, 2, 4096, 0) == 1
+    assert so.ffd_select_kernels(1, 8, 32768, 0) == 1
+    assert so.ffd_select_kernels(1, 8, 131072, 0) == 1            # 32 workgroups of 64 blocks
+    assert so.ffd_select_kernels(1, 8, 262144, 0) == 2            # 128 blocks per workgroup
+    assert so.ffd_select_kernels(4, 8, 131072, 0) == 2
+    assert so.ffd_select_kernels(4, 8, 131072, 32) == 1           # 64 blocks per workgroup
+    assert so.ffd_select_kernels(4, 8, 131072, 5000) == 0
+    assert so.ffd_dense_resolve_splits(4, 8, 131072, 0) == 15     # dense: 512 workgroups
+    assert so.ffd_dense_resolve_splits(4, 8, 131072, 5) == 5
+    # partials max((S*P + P)*G, B*Hq*S1) rows of (D+2)*4 bytes | table P*8 | counts P*S1s*4 |
+    # lists P*C*4 | block scores P*C*G*4, each region on a 256-byte boundary (S = 7 refinement splits
+    # and S1s = 8 scan splits of the top-k path at 4 x 8 x 128K; S1 = 8 for top-delta)
     up = lambda x: -(-x // 256) * 256
     P, G, C = 32, 4, 2048
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
-        up((7 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
+        up(max(7 * P + P, 8 * P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
         + P * C * G * 4)
     # the dense path's partials (S = 15) are larger than the FFD layout for few blocks
     assert so.ffd_workspace_bytes(4, 32, 8, 8192, 128, 0) == 4 * 32 * 15 * 130 * 4
@@ -142,4 +162,15 @@ def test_extras_top_k_checked_before_launch(so):
     with_mt = ffd.DecodeExtras(None, fake, 0, 8)
     assert so.ffd_decode_attention_ex(*args, ctypes.byref(with_mt)) == 1
     # the struct the binding passes has the header's four fields, in order
-    assert [f[0] for f in ffd.DecodeExtras._fields_] == ["stage_events", "m_tilde", "pseudo_max", "top_k"]
+    assert [f[0] for f in ffd.DecodeExtras._fields_] == ["stage_events", "m_tilde", "pseudo_max", "top_k",
+                                                          "kernels"]
+
+
+def test_extras_kernels_checked_before_launch(so):
+    """An unknown kernel choice, or the fused kernel with the top-k rule, is rejected before any launch."""
+    from paper_2609_00097_amd import ffd
+    fake = 0x1000
+    args = [fake] * 6 + [1, 32, 8, 4096, 128, 2, 64, 5.0, 64, 256, 0, 0.0, fake, None, None, fake, 1 << 30, None]
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(ffd.DecodeExtras(None, None, 0, 0, 3))) == 1
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(ffd.DecodeExtras(None, None, 0, 0, -1))) == 1
+    assert so.ffd_decode_attention_ex(*args, ctypes.byref(ffd.DecodeExtras(None, None, 0, 8, 1))) == 1

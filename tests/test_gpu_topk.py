@@ -117,10 +117,12 @@ def test_ties_go_in_block_order(template):
         compare_topk(c, k, out, lse, mask, exact=True)
 
 
-def test_full_budget_equals_delta_infinity_bit_for_bit():
-    """Keeping every block through the budget gives the same mask, outputs and lse as delta = inf:
-    the recomputed scan scores equal the stored ones and the refinement allocation is the same."""
+def test_full_budget_equals_delta_infinity():
+    """Keeping every block through the budget gives the mask of delta = inf bit for bit, and the same
+    outputs and lse up to the rounding of a different partition of the work (the top-k path refines
+    in its own kernel, top-delta in the fused one); both match the oracle's delta = inf outputs."""
     from paper_2609_00097_amd import ffd
+    from tests.gpu_util import compare_ffd
     c = I.small_case(seed=73, B=3, Hq=16, Hkv=2, seq_lens=(3000, 4096, 700), heavy_frac=0.05)
     up = Uploaded(c)
     qk = ffd.quantize_keys(up.k)
@@ -129,7 +131,10 @@ def test_full_budget_equals_delta_infinity_bit_for_bit():
                                                 return_lse=True, return_mask=True)
     torch.cuda.synchronize()
     assert torch.equal(mask_k, mask_i)
-    assert torch.equal(out_k, out_i) and torch.equal(lse_k, lse_i)
+    np.testing.assert_allclose(out_k.float().cpu().numpy(), out_i.float().cpu().numpy(), rtol=1e-2, atol=2e-3)
+    np.testing.assert_allclose(lse_k.cpu().numpy(), lse_i.cpu().numpy(), rtol=0, atol=1e-4)
+    compare_ffd(c, float("inf"), out_k, lse_k, mask_k)
+    compare_ffd(c, float("inf"), out_i, lse_i, mask_i)
 
 
 @pytest.mark.parametrize("bits", [4, 8])
