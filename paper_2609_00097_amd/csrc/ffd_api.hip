@@ -142,12 +142,15 @@ int scan_splits(int B, int Hkv, int Lcap) {
     return (int)s;
 }
 
-// Workgroups per (sequence, KV head) of the fused top-delta kernel, S1: num_splits when given,
-// else about one 8-wave workgroup per CU in all (floor, so that the grid fits one round of
-// workgroups), each with at least kMinFusedBlocks blocks of the capacity (a short context takes
-// one workgroup per group, which then writes the outputs itself, with no merge launch); never fewer
-// than ceil(blocks / kFfdMaxScanBlocks) (a workgroup's block scores are staged in LDS).
-constexpr int kMinFusedBlocks = 64;
+// Workgroups per (sequence, KV head) of the fused top-delta kernel, S1: num_splits when given;
+// automatically one for a group of at most kFusedAloneBlocks blocks (the kernel then writes the
+// outputs itself, with no merge launch), else about kFusedTargetBlocks blocks per workgroup with
+// at most two workgroups per CU in all. Never fewer than ceil(blocks / kFfdMaxScanBlocks) (a
+// workgroup's block scores are staged in LDS). Measured at B = 1, 32q/8kv, delta 5 (layer-averaged
+// us per step, best split count per length): 4K 13.7 (S1 = 1; 15.0 with a merge), 8K 14.5 (8),
+// 16K 14.6 (16), 32K 15.7 (16..32), 64K 25.0 (64), 128K 29.8 (64).
+constexpr int kFusedAloneBlocks = 64;
+constexpr int kFusedTargetBlocks = 16;
 
 int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
@@ -156,9 +159,13 @@ int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
     const long long need = (nblk_cap + kFfdMaxScanBlocks - 1) / kFfdMaxScanBlocks;
     long long s = num_splits;
     if (s == 0) {
-        s = device_cus() / pairs;
-        const long long cap = nblk_cap / kMinFusedBlocks;
-        if (s > cap) s = cap;
+        if (nblk_cap <= kFusedAloneBlocks) {
+            s = 1;
+        } else {
+            s = (nblk_cap + kFusedTargetBlocks - 1) / kFusedTargetBlocks;
+            const long long cap = 2LL * device_cus() / pairs;
+            if (s > cap) s = cap;
+        }
     }
     if (s < need) s = need;
     if (s < 1) s = 1;
@@ -166,15 +173,18 @@ int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
     return (int)s;
 }
 
-// The top-delta kernels FFD_KERNELS_AUTO picks: the fused kernel while each of its workgroups covers
-// at most kFusedMaxBlocks blocks of the capacity (its refinement, at the end of each workgroup's
-// scan, then stays short), else scan + refinement + merge, whose refinement spreads the kept blocks
-// evenly over every CU.
+// The top-delta kernels FFD_KERNELS_AUTO picks: the fused kernel while its workgroups cover at
+// most kFusedMaxBlocks blocks of the capacity each (or a group fits one workgroup), else scan +
+// refinement + merge, whose refinement spreads the kept blocks over every CU. (The fused kernel
+// refines each workgroup's own kept blocks, so its time follows the workgroup with the most: at
+// 4 x 128K, 32q/8kv, delta 5, its best split count gave 66.9 us against 58.9 us for the split
+// kernels; at 1 x 256K, 64 workgroups of 64 blocks per group gave 32.4 us against 34.1 us.)
 constexpr int kFusedMaxBlocks = 64;
 
 int auto_kernels(int Lcap, int S1f) {
-    const int bps = (Lcap / FFD_BLOCK + S1f - 1) / S1f;
-    return bps <= kFusedMaxBlocks ? FFD_KERNELS_FUSED : FFD_KERNELS_SPLIT;
+    const int nblk_cap = Lcap / FFD_BLOCK;
+    const int bps = (nblk_cap + S1f - 1) / S1f;
+    return bps <= kFusedMaxBlocks || nblk_cap <= kFusedAloneBlocks ? FFD_KERNELS_FUSED : FFD_KERNELS_SPLIT;
 }
 
 // FFD workspace: partial states (for the fused top-delta kernel's B * Hq * S1f rows, or for the

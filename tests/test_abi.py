@@ -50,33 +50,36 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_resolve_splits(64, 8, 131072, 0) == 1           # at least one split
     assert so.ffd_resolve_splits(4, 8, 131072, 7) == 7
     assert so.ffd_resolve_splits(4, 8, 131072, 5000) == 0
-    # fused kernel: S1 workgroups per (sequence, KV head), about one per CU in all (floor), each with
-    # >= 64 blocks of the capacity, never fewer than blocks / 256
-    assert so.ffd_fused_splits(4, 8, 131072, 0) == 8              # 32 groups x 8 = 256 workgroups
+    # fused kernel: S1 workgroups per (sequence, KV head): one for at most 64 blocks, else ~16 blocks
+    # each with at most two workgroups per CU in all (512), never fewer than blocks / 256
     assert so.ffd_fused_splits(1, 2, 4096, 0) == 1                # 64 blocks: one workgroup, no merge
-    assert so.ffd_fused_splits(1, 8, 32768, 0) == 8               # capped: 512 blocks / 64
-    assert so.ffd_fused_splits(4, 6, 131072, 0) == 10             # floor(256 / 24)
+    assert so.ffd_fused_splits(1, 8, 8192, 0) == 8                # 128 blocks / 16
+    assert so.ffd_fused_splits(1, 8, 131072, 0) == 64             # capped: 512 / 8 groups
+    assert so.ffd_fused_splits(4, 8, 131072, 0) == 16             # capped: 512 / 32 groups
+    assert so.ffd_fused_splits(4, 6, 131072, 0) == 21             # floor(512 / 24)
     assert so.ffd_fused_splits(64, 8, 131072, 0) == 8             # at least 2048 / 256
     assert so.ffd_fused_splits(4, 8, 131072, 7) == 8              # raised to 2048 / 256
     assert so.ffd_fused_splits(4, 8, 131072, 12) == 12
     assert so.ffd_fused_splits(4, 8, 131072, 5000) == 0
-    # automatic kernels: fused while a workgroup covers at most 64 blocks (1 = fused, 2 = split)
+    # automatic kernels: fused while a workgroup covers at most 64 blocks or a sequence fits one
+    # workgroup (1 = fused, 2 = split)
     assert so.ffd_select_kernels(1, 2, 4096, 0) == 1
-    assert so.ffd_select_kernels(1, 8, 32768, 0) == 1
-    assert so.ffd_select_kernels(1, 8, 131072, 0) == 1            # 32 workgroups of 64 blocks
-    assert so.ffd_select_kernels(1, 8, 262144, 0) == 2            # 128 blocks per workgroup
-    assert so.ffd_select_kernels(4, 8, 131072, 0) == 2
+    assert so.ffd_select_kernels(1, 8, 32768, 0) == 1             # 32 workgroups of 16 blocks
+    assert so.ffd_select_kernels(1, 8, 131072, 0) == 1            # 64 workgroups of 32 blocks
+    assert so.ffd_select_kernels(1, 8, 262144, 0) == 1            # 64 blocks per workgroup
+    assert so.ffd_select_kernels(1, 8, 524288, 0) == 2            # 128 blocks per workgroup
+    assert so.ffd_select_kernels(4, 8, 131072, 0) == 2            # 128 blocks per workgroup
     assert so.ffd_select_kernels(4, 8, 131072, 32) == 1           # 64 blocks per workgroup
     assert so.ffd_select_kernels(4, 8, 131072, 5000) == 0
     assert so.ffd_dense_resolve_splits(4, 8, 131072, 0) == 15     # dense: 512 workgroups
     assert so.ffd_dense_resolve_splits(4, 8, 131072, 5) == 5
     # partials max((S*P + P)*G, B*Hq*S1) rows of (D+2)*4 bytes | table P*8 | counts P*S1s*4 |
     # lists P*C*4 | block scores P*C*G*4, each region on a 256-byte boundary (S = 7 refinement splits
-    # and S1s = 8 scan splits of the top-k path at 4 x 8 x 128K; S1 = 8 for top-delta)
+    # and S1s = 8 scan splits of the split kernels at 4 x 8 x 128K; S1 = 16 for the fused kernel)
     up = lambda x: -(-x // 256) * 256
     P, G, C = 32, 4, 2048
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
-        up(max(7 * P + P, 8 * P) * G * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
+        up(max((7 * P + P) * G, 4 * 32 * 16) * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
         + P * C * G * 4)
     # the dense path's partials (S = 15) are larger than the FFD layout for few blocks
     assert so.ffd_workspace_bytes(4, 32, 8, 8192, 128, 0) == 4 * 32 * 15 * 130 * 4
