@@ -335,7 +335,9 @@ size_t ffd_dense_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int nu
     if (check_shapes(B, Hq, Hkv, Lcap, D) != FFD_OK) return 0;
     const int S = resolve_splits(B > 0 ? B : 1, Hkv, Lcap, num_splits, true);
     if (S <= 0) return 0;
-    return partials_bytes(B, Hq, S, D);
+    if (B > kDenseBalanceMaxSeqs) return partials_bytes(B, Hq, S, D);
+    // balanced mode: (S + 1) partial rows per head, then the per-(sequence, KV head) table
+    return round_up(partials_bytes(B, Hq, S + 1, D), kAlign) + (size_t)B * Hkv * sizeof(int2);
 }
 
 size_t ffd_workspace_bytes(int B, int Hq, int Hkv, int Lcap, int D, int num_splits) {
@@ -539,10 +541,14 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
         return FFD_ERR_WORKSPACE_TOO_SMALL;
     const int G = Hq / Hkv;
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
-    const Partials P = carve(workspace, B, Hq, S);
+    const bool balanced = B <= kDenseBalanceMaxSeqs;
+    const Partials P = carve(workspace, B, Hq, balanced ? S + 1 : S);
+    int2* table = balanced ? reinterpret_cast<int2*>(static_cast<uint8_t*>(workspace) +
+                                                     round_up(partials_bytes(B, Hq, S + 1, D), kAlign))
+                           : nullptr;
     DenseArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                static_cast<const uint16_t*>(v), seq_lens, P.m, P.l, P.acc, Hq, Hkv, Lcap, G, S, scale};
-    const dim3 grid((unsigned)S, (unsigned)Hkv, (unsigned)B);
+                static_cast<const uint16_t*>(v), seq_lens, P.m, P.l, P.acc, table, B, Hq, Hkv, Lcap, G, S, scale};
+    const dim3 grid = balanced ? dim3((unsigned)((S + 1) * B * Hkv)) : dim3((unsigned)S, (unsigned)Hkv, (unsigned)B);
     if (G <= 4)
         hipLaunchKernelGGL(dense_decode_kernel<1>, grid, dim3(kThreads), 0, stream, a);
     else
@@ -550,7 +556,7 @@ int ffd_dense_decode_attention(const void* q, const void* k, const void* v, cons
     st = launch_status();
     if (st != FFD_OK) return st;
     hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(B * Hq)), dim3(kThreads), 0, stream, P.m, P.l,
-                       P.acc, S, nullptr, 1, static_cast<uint16_t*>(out), lse);
+                       P.acc, S, table, balanced ? G : 1, static_cast<uint16_t*>(out), lse);
     return launch_status();
 }
 

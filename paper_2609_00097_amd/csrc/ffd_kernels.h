@@ -85,6 +85,13 @@ struct TopkArgs {
     int Hq, Hkv, Lcap, S1, k;
 };
 
+// Dense decode. Balanced mode (table != null, B <= kDenseBalanceMaxSeqs): a 1-D grid of
+// (S + 1) * B * Hkv workgroups; sequence b (n_b blocks) gets W_b = ceil(n_b * min(W, N) / N)
+// workgroups per KV head (W = S * B * Hkv, N = Hkv * sum n_b; 1 for an empty sequence), numbered in
+// (sequence, KV head) order, each taking an equal run of the sequence's blocks and writing its
+// partial rows at its own index (table[b * Hkv + kvh] = first workgroup, count). Otherwise a grid
+// (S, Hkv, B) of equal runs per sequence with rows [B, Hq, S].
+constexpr int kDenseBalanceMaxSeqs = 256;
 struct DenseArgs {
     const uint16_t* q;          // bf16 [B, Hq, 128]
     const uint16_t* k;          // bf16 [B, Hkv, Lcap, 128]
@@ -93,7 +100,8 @@ struct DenseArgs {
     float* part_m;
     float* part_l;
     float* part_acc;
-    int Hq, Hkv, Lcap, G, S;
+    int2* table;                // balanced mode: [B * Hkv] (first workgroup, workgroups); else null
+    int B, Hq, Hkv, Lcap, G, S;
     float scale;
 };
 

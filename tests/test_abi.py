@@ -81,14 +81,18 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 128, 0) == (
         up(max((7 * P + P) * G, 4 * 32 * 16) * 130 * 4) + up(P * 8) + up(P * 8 * 4) + up(P * C * 4)
         + P * C * G * 4)
-    # the dense path's partials (S = 15) are larger than the FFD layout for few blocks
-    assert so.ffd_workspace_bytes(4, 32, 8, 8192, 128, 0) == 4 * 32 * 15 * 130 * 4
+    # the dense path's balanced partials (S + 1 = 16 rows per head) and table are larger than the FFD
+    # layout for few blocks
+    dense = up(4 * 32 * 16 * 130 * 4) + 32 * 8
+    assert so.ffd_workspace_bytes(4, 32, 8, 8192, 128, 0) == dense
     P, G, C = 2, 8, 64
     assert so.ffd_workspace_bytes(1, 16, 2, 4096, 128, 3) == (
         up((3 * P + P) * G * 130 * 4) + up(P * 8) + up(P * 4 * 4) + up(P * C * 4)
         + P * C * G * 4)
     assert so.ffd_workspace_bytes(1, 8, 8, 1 << 25, 128, 1) == 0         # Lcap beyond 2^24 tokens
-    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 128, 0) == 4 * 32 * 15 * 130 * 4
+    assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 128, 0) == dense
+    # more than 256 sequences: equal runs per sequence, S rows per head and no table
+    assert so.ffd_dense_workspace_bytes(300, 8, 8, 4096, 128, 1) == 300 * 8 * 1 * 130 * 4
     assert so.ffd_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
     assert so.ffd_dense_workspace_bytes(4, 32, 8, 131072, 96, 0) == 0
 

@@ -51,3 +51,23 @@ def test_full_size_workload3_sampled():
     print(f"case {c.name} seed {c.seed}", flush=True)
     out, lse = _dense(Uploaded(c))
     compare_dense(c, out, lse, heads=[(0, 0), (3, 7), (2, 4)])
+
+
+def test_full_size_ragged_workload5_sampled():
+    """The ragged batch of 16 sequences (8K..128K): workgroups are given to the sequences in
+    proportion to their blocks; oracle on sampled pairs, the shortest and the longest included."""
+    c = I.workload(5)
+    order = np.argsort(c.seq_lens)
+    heads = [(int(order[0]), 0), (int(order[-1]), 7), (int(order[len(order) // 2]), 3)]
+    print(f"case {c.name} seed {c.seed} pairs {heads}", flush=True)
+    out, lse = _dense(Uploaded(c))
+    compare_dense(c, out, lse, heads=heads)
+
+
+def test_more_sequences_than_the_balanced_mode_takes():
+    """300 sequences (more than 256): equal runs per sequence instead of the balanced allocation."""
+    lens = [1 + (53 * b) % 700 for b in range(300)]
+    c = I.small_case(seed=37, B=300, Hq=4, Hkv=1, seq_lens=lens, Lcap=704, heavy_frac=0.0)
+    print("case dense 300 sequences", flush=True)
+    out, lse = _dense(Uploaded(c), 2)
+    compare_dense(c, out, lse, heads=[(0, 0), (1, 0), (150, 0), (299, 0)])
