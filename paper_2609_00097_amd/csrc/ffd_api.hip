@@ -271,9 +271,9 @@ void launch_fused(int bits, int nt, int mode, dim3 grid, hipStream_t stream, con
 // The refinement kernel, recomputing the scan scores from rbits-bit codes.
 template <int NT>
 void launch_refine_nt(int rbits, dim3 grid, hipStream_t stream, const RefineArgs& ra) {
-    if (rbits == 2) hipLaunchKernelGGL((ffd_refine_kernel<NT, 2>), grid, dim3(kThreads), 0, stream, ra);
-    else if (rbits == 4) hipLaunchKernelGGL((ffd_refine_kernel<NT, 4>), grid, dim3(kThreads), 0, stream, ra);
-    else hipLaunchKernelGGL((ffd_refine_kernel<NT, 8>), grid, dim3(kThreads), 0, stream, ra);
+    if (rbits == 2) hipLaunchKernelGGL((ffd_refine_kernel<NT, 2>), grid, dim3(kRefineThreads), 0, stream, ra);
+    else if (rbits == 4) hipLaunchKernelGGL((ffd_refine_kernel<NT, 4>), grid, dim3(kRefineThreads), 0, stream, ra);
+    else hipLaunchKernelGGL((ffd_refine_kernel<NT, 8>), grid, dim3(kRefineThreads), 0, stream, ra);
 }
 
 // Every argument check of ffd_decode_attention_ex, in its order, with nothing launched; with

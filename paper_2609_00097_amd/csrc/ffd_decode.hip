@@ -19,20 +19,27 @@
 // Output register i of lane (g, n) is row 4g + i, column n: head g's limbs for token n, so each
 // 16-lane row group owns one head and a tile's maximum is a 16-lane DPP reduction.
 //
-// Two kernels, so that each stage's HBM stream is balanced over the whole chip:
-//  * ffd_scan_kernel streams the codes and absmaxes of every block once (the dominant, perfectly
-//    regular stream; one 8-wave workgroup per CU whose waves take blocks from an LDS counter), keeps
-//    each block's per-head maximum score in LDS and, once its stream and the pseudo-max are done,
-//    takes the keep decision per (head, block): the kept blocks, with their per-head keep bits, form
-//    its workgroup's kept list (in block order) in the workspace, plus the list's length.
-//  * ffd_refine_kernel gives each (sequence, KV head) a number of workgroups proportional to its
-//    kept blocks (every workgroup computes the same allocation from the scan's counts, so no
-//    cross-workgroup synchronisation is needed); each workgroup refines an equal share of its KV
-//    group's kept blocks, wave w taking 16-token tile w of every block, with several tiles' residual
-//    and value loads in flight, recomputes the scan scores s_hat of each tile from its codes (Eq. 4's
-//    reuse term: the same integer MFMA and fp32 operations as the scan, so the same values; storing
-//    them would cost as many bytes, written then read), and writes one partial (m, l, acc) per head.
-//    lse_merge_kernel combines the partials of each head, located through a small per-group table.
+// Two ways to run a step, chosen by the host (FFD_KERNELS_*):
+//  * ffd_decode_kernel, the fused kernel (short and mid contexts: at most 64 blocks per
+//    workgroup): S1 workgroups per (sequence, KV head) each scan an interleaved share of the group's
+//    blocks (j = s + S1 i), decide them, and refine and attend their own kept blocks; one partial
+//    state per head (or, with S1 = 1, the outputs themselves).
+//  * the split kernels, where the kept blocks are too many for their owners to refine in time:
+//    - ffd_scan_kernel streams the codes and absmaxes of every block once (the dominant, perfectly
+//      regular stream; one 8-wave workgroup per CU whose waves take blocks from an LDS counter),
+//      keeps each block's per-head maximum score in LDS and, once its stream and the pseudo-max are
+//      done, takes the keep decision per (head, block): the kept blocks, with their per-head keep
+//      bits, form its workgroup's kept list (in block order) in the workspace, plus the list's
+//      length;
+//    - ffd_refine_kernel gives each (sequence, KV head) a number of workgroups proportional to its
+//      kept blocks (every workgroup computes the same allocation from the scan's counts, so no
+//      cross-workgroup synchronisation is needed); each 8-wave workgroup refines an equal share of
+//      its group's kept blocks, wave w taking 16-token tile w % 4 of every other block, with
+//      several tiles' residual and value loads in flight, and writes one partial (m, l, acc) per
+//      head; lse_merge_kernel combines the partials of each head through a small per-group table.
+// Both recompute the scan scores s_hat of each kept tile from its codes (Eq. 4's reuse term: the
+// same integer MFMA and fp32 operations as the scan, so the same values; storing them would cost
+// as many bytes, written then read).
 #include "ffd_device.h"
 #include "ffd_kernels.h"
 
@@ -45,9 +52,6 @@ namespace {
 #endif
 #ifndef FFD_REFINE_RING
 #define FFD_REFINE_RING 2
-#endif
-#ifndef FFD_REFINE_OCC
-#define FFD_REFINE_OCC 2
 #endif
 constexpr int kRing2 = FFD_SCAN_RING;         // 2-bit scan loads in flight per wave (blocks)
 constexpr int kRefineRing = FFD_REFINE_RING;  // refinement tiles in flight per wave
@@ -372,15 +376,15 @@ constexpr int kCountCache = 4096;            // scan counts kept in LDS when the
 template <int NT>
 struct RefineLds {
     QueryLds<NT> qs;
-    int wsum[2][kWaves];                 // wg_exclusive_scan scratch, alternating halves
+    int wsum[2][kRefineWaves];           // wg_exclusive_scan scratch, alternating halves
     int sel[4];                          // this workgroup's KV group: pair, first workgroup, workgroups, kept
     int pn[kPairChunk];                  // kept blocks per KV group of the current pass (large inputs)
     int cnt[kCountCache + 1];            // exclusive prefix of all scan counts, when they fit
     int pref[kFfdMaxScanSplits + 1];     // exclusive prefix of the group's per-split counts (large inputs)
-    TileP<NT> tp[kWaves];
+    TileP<NT> tp[kRefineWaves];
     union {
         uint32_t list[kChunk];           // kept blocks of the share: j | keep bits << 24
-        EpilogueLds<NT> epi;
+        EpilogueLds<NT, kRefineWaves> epi;
     } u;
 };
 
@@ -908,11 +912,13 @@ __global__ __launch_bounds__(kScanThreads, 1) void ffd_decode_kernel(FusedArgs a
 // group's exit.
 // ================================================================================================
 template <int NT, int RBITS>
-__global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(RefineArgs a) {
+__global__ __launch_bounds__(kRefineThreads, 1) void ffd_refine_kernel(RefineArgs a) {
     __shared__ RefineLds<NT> sm;
     const int wg = blockIdx.x;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 4, n = lane & 15;
+    constexpr int kPar = kRefineWaves / 4;          // waves per tile index
+    const int T4 = wave & 3, par = wave >> 2;       // tile T4 of the share's entries par, par + kPar, ...
     const int G = a.G, S1 = a.S1, npairs = a.npairs;
 
     // ---- allocation: total kept N, then this workgroup's KV group ---------------------------
@@ -928,7 +934,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     const bool cached = total <= kCountCache && npairs <= kPairChunk;
     int N = 0, running = 0, half = 0;
     auto scan = [&](int v, int* tot) {
-        const int e = wg_exclusive_scan(v, sm.wsum[half], tot);
+        const int e = wg_exclusive_scan<kRefineWaves>(v, sm.wsum[half], tot);
         half ^= 1;
         return e;
     };
@@ -1037,14 +1043,14 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         }
     } else {
         int part = 0;
-        for (int i = tid; i < total; i += kThreads) part += a.counts[i];
+        for (int i = tid; i < total; i += kRefineThreads) part += a.counts[i];
         (void)scan(part, &N);
         const long long Weff = min(W, (long long)max(N, 1));
         for (int c0 = 0; c0 < npairs; c0 += kPairChunk) {
             const int np = min(kPairChunk, npairs - c0);
-            for (int i = tid; i < np; i += kThreads) sm.pn[i] = 0;
+            for (int i = tid; i < np; i += kRefineThreads) sm.pn[i] = 0;
             __syncthreads();
-            for (int i = tid; i < np * S1; i += kThreads) {
+            for (int i = tid; i < np * S1; i += kRefineThreads) {
                 const int c = a.counts[(size_t)c0 * S1 + i];
                 if (c) atomicAdd(&sm.pn[i / S1], c);
             }
@@ -1117,7 +1123,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     // pref(s) <= r < pref(s + 1), at list position s * bps + r - pref(s)
     if (!cached) {
         int run = 0;
-        for (int c0 = 0; c0 < S1; c0 += kThreads) {
+        for (int c0 = 0; c0 < S1; c0 += kRefineThreads) {
             const int sidx = c0 + tid;
             const int c = sidx < S1 ? a.counts[bh * S1 + sidx] : 0;
             int tot = 0;
@@ -1147,13 +1153,13 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
     for (int t = 0; t < NT; ++t) { m_run[t] = -INFINITY; l_part[t] = 0.f; }
     TileP<NT>& tp = sm.tp[wave];
 
-    // refine (Eq. 4) and attend tile `wave` of one kept block
+    // refine (Eq. 4) and attend tile T4 of one kept block
     auto attend = [&](const RefineTile<NT, RBITS>& rt, int j, uint32_t bits) {
         float z[NT];
         bool keep[NT];
         const float Mt = bf16_to_f32((uint16_t)rt.m);
         float shat[NT];                             // Eq. 4's first term: the scan scores, recomputed
-        tile_scores<NT, RBITS>(rt.cw, Mt, 64 * j + 16 * wave + n < L, hc, shat);
+        tile_scores<NT, RBITS>(rt.cw, Mt, 64 * j + 16 * T4 + n < L, hc, shat);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             v4i acc = {0, 0, 0, 0};
@@ -1170,25 +1176,34 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         wave_lds_fence();
     };
 
-    // the m list entries staged in LDS: gather with kRefineRing tiles in flight. The refill of the
-    // last round re-reads the share's last tile (clamped): it is still cached, and a conditional
-    // refill would cost more registers than it saves. fast_consts: the query constants are built by
-    // this wave while the first tiles are in flight.
+    // the m list entries staged in LDS: this wave takes tile T4 of entries par, par + kPar, ... with
+    // kRefineRing tiles in flight. The refill of the last round re-reads the wave's last tile
+    // (clamped): it is still cached, and a conditional refill would cost more registers than it
+    // saves. fast_consts: the query constants are built by this wave while its first tiles are in
+    // flight.
     auto refine_entries = [&](int m, bool fast_consts) {
-        auto block_of = [&](int i) { return (int)(sm.u.list[min(i, m - 1)] & 0xffffffu); };
+        const int mine = m > par ? (m - par + kPar - 1) / kPar : 0;
+        if (mine == 0) {                            // wave-uniform
+            if (fast_consts) build_query_consts_wave<NT>(sm.qs, qa, G, a.scale, a.top_level, lane, hc);
+            return;
+        }
+        auto entry = [&](int k) { return sm.u.list[par + kPar * min(k, mine - 1)]; };
         RefineTile<NT, RBITS> ring[kRefineRing];
 #pragma unroll
         for (int r = 0; r < kRefineRing; ++r)
-            ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh, block_of(r), wave,
-                                                  lane, L);
+            ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh,
+                                                  (int)(entry(r) & 0xffffffu), T4, lane, L);
         if (fast_consts) build_query_consts_wave<NT>(sm.qs, qa, G, a.scale, a.top_level, lane, hc);
-        for (int i0 = 0; i0 < m; i0 += kRefineRing) {
+        for (int k0 = 0; k0 < mine; k0 += kRefineRing) {
 #pragma unroll
             for (int r = 0; r < kRefineRing; ++r) {
-                const int i = i0 + r;
-                if (i < m) attend(ring[r], (int)(sm.u.list[i] & 0xffffffu), sm.u.list[i] >> 24);
+                const int k = k0 + r;
+                if (k < mine) {
+                    const uint32_t e = entry(k);
+                    attend(ring[r], (int)(e & 0xffffffu), e >> 24);
+                }
                 ring[r] = load_refine_tile<NT, RBITS>(resid_bh, v_bh, codes_bh, absmax_bh,
-                                                      block_of(i + kRefineRing), wave, lane, L);
+                                                      (int)(entry(k + kRefineRing) & 0xffffffu), T4, lane, L);
             }
         }
     };
@@ -1216,7 +1231,7 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         bool consts_ready = false;
         for (int c = r0; c < r1; c += kChunk) {
             const int m = min(kChunk, r1 - c);
-            for (int i = tid; i < m; i += kThreads) sm.u.list[i] = list_entry(c + i);
+            for (int i = tid; i < m; i += kRefineThreads) sm.u.list[i] = list_entry(c + i);
             if (!consts_ready) {                    // the query loads and the list loads overlap
                 build_query_consts<NT>(sm.qs, qw, G, a.scale, a.top_level, tid, hc);
                 consts_ready = true;
@@ -1228,8 +1243,8 @@ __global__ __launch_bounds__(kThreads, FFD_REFINE_OCC) void ffd_refine_kernel(Re
         if (!consts_ready) __syncthreads();
     }
 
-    write_partials<NT>(sm.u.epi, pv, m_run, l_part, wave, lane, G, (size_t)wg * G, 1, a.part_m,
-                       a.part_l, a.part_acc);
+    write_partials<NT, kRefineWaves>(sm.u.epi, pv, m_run, l_part, wave, lane, G, (size_t)wg * G, 1,
+                                     a.part_m, a.part_l, a.part_acc);
 }
 
 template __global__ void ffd_scan_kernel<1, 2, kSelThumbnailPM>(ScanArgs);

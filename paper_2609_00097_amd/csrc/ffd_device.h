@@ -103,6 +103,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 // Exclusive prefix sum over the workgroup (thread order) of x; *total receives the sum. One
 // barrier: consecutive calls must alternate between the two halves of wsum[2][kWaves] (a wave
 // reaching call k + 2 has passed call k + 1's barrier, so every wave has read call k's half).
+template <int NW = kWaves>
 __device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = x;
@@ -115,7 +116,7 @@ __device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
     __syncthreads();
     int before = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
         const int s = wsum[w];
         before += w < wave ? s : 0;
         tot += s;
