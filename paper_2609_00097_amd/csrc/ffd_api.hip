@@ -57,10 +57,12 @@ void* device_scratch() {
 // equal work; it should not exceed one per CU, because a CU serves its older workgroup's memory
 // requests first, so a second workgroup on a CU finishes its share about 3 us later (at 4 x 128K on
 // 256 CUs, delta 5: S = 7 (256 workgroups) 60.0 us per step; S = 8 (288) 65.2 us; S = 15 (512)
-// 62.2 us; S = 6 (224) 62.3 us). The dense path keeps two workgroups per CU, its best split count
-// (S = 7 measured 1 % slower at 4 x 128K).
+// 62.2 us; S = 6 (224) 62.3 us). The dense path keeps two workgroups per CU for up to 63 KV groups
+// (4 x 128K: S = 15, 512 workgroups, against S = 23 or 31 about 2 % slower; B = 1: more splits are
+// slower still) and three from 64 groups on (the ragged batch of 16 sequences, 128 groups: 512
+// workgroups 873 us, 768 workgroups 833 us, 1024 workgroups 832 us).
 int ffd_target_workgroups() { return device_cus(); }
-int dense_target_workgroups() { return 2 * device_cus(); }
+int dense_target_workgroups(long long pairs) { return (pairs >= 64 ? 3 : 2) * device_cus(); }
 constexpr int kMinBlocksPerSplit = 8;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -68,8 +70,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int resolve_splits(int B, int Hkv, int Lcap, int num_splits, bool dense = false) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
     if (num_splits > 0) return num_splits;
-    const int target = dense ? dense_target_workgroups() : ffd_target_workgroups();
     const long long pairs = (long long)B * Hkv;
+    const int target = dense ? dense_target_workgroups(pairs) : ffd_target_workgroups();
     long long s = target / pairs - 1;
     const long long cap = (long long)(Lcap / FFD_BLOCK) / kMinBlocksPerSplit;
     if (s > cap) s = cap;

@@ -73,6 +73,8 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_select_kernels(4, 8, 131072, 5000) == 0
     assert so.ffd_dense_resolve_splits(4, 8, 131072, 0) == 15     # dense: 512 workgroups
     assert so.ffd_dense_resolve_splits(4, 8, 131072, 5) == 5
+    assert so.ffd_dense_resolve_splits(16, 8, 131072, 0) == 5     # 128 KV groups: 768 workgroups
+    assert so.ffd_dense_resolve_splits(8, 8, 131072, 0) == 11     # 64 KV groups: 768 workgroups
     # partials max((S*P + P)*G, B*Hq*S1) rows of (D+2)*4 bytes | table P*8 | counts P*S1s*4 |
     # lists P*C*4 | block scores P*C*G*4, each region on a 256-byte boundary (S = 7 refinement splits
     # and S1s = 8 scan splits of the split kernels at 4 x 8 x 128K; S1 = 16 for the fused kernel)
