@@ -1,7 +1,8 @@
 """Benchmark of one FFD decode step on one MI355X, with the dense flash-decode baseline beside it.
 
 A step is one ffd_decode_attention call (scan + top-delta decision, refinement + online
-softmax . V, split merge: three kernels) over one batch of synthetic inputs already resident in
+softmax . V, split merge; the library runs them as the fused kernel, plus the merge when a head
+has several slices, or as three kernels) over one batch of synthetic inputs already resident in
 HBM. The headline protocol is the paper's layer-averaged setting (Sec. 4.2): the device holds
 ``--layers`` N distinct copies of the whole cache (one per layer: quantized keys, values, and the
 bf16 keys the dense baseline reads), and the timed steps run back to back, step i on layer

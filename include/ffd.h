@@ -14,8 +14,11 @@
  *                               scan score of a kept token is recomputed from its codes, bit for bit
  *                               the scan's value, rather than stored), online-softmax attention over
  *                               the kept blocks, split into partial states merged by log-sum-exp
- *                               (flash-decoding, Sec. 2 and Sec. 3.3). Three kernels in order on
- *                               `stream`: scan + selection, refinement + attention, merge.
+ *                               (flash-decoding, Sec. 2 and Sec. 3.3). Kernels in order on `stream`:
+ *                               either one fused kernel (scan, selection, refinement and attention
+ *                               per interleaved slice of a sequence; short and mid contexts) plus
+ *                               the merge when a head has more than one slice, or scan + selection,
+ *                               refinement + attention spread over every CU, merge.
  *   ffd_dense_decode_attention  exact dense decode attention over the bf16 cache (the dense
  *                               comparator of Sec. 4.2), same split-and-merge scheme.
  *
