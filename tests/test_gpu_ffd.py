@@ -226,10 +226,10 @@ def _full_size(wl, delta, heads, kernels="auto"):
     (3, 7.0, lambda c: _largest_planted(c, 3) + [(1, 1)], "auto"),
     (3, 5.0, lambda c: _largest_planted(c, 2) + [(0, 3)], "fused"),
     (4, 5.0, [(0, h) for h in range(8)], "auto"),
-    (4, 5.0, [(0, 1), (0, 6)], "fused"),
+    (4, 5.0, [(0, 1), (0, 6)], "split"),
     (5, 5.0, [(0, 0), (1, 2), (6, 5), (15, 7)], "auto"),
     (5, 5.0, [(1, 0), (8, 4)], "fused"),
-], ids=["wl3-d5", "wl3-d3", "wl3-d7", "wl3-d5-fused", "wl4-d5-all-heads", "wl4-d5-fused", "wl5-d5",
+], ids=["wl3-d5", "wl3-d3", "wl3-d7", "wl3-d5-fused", "wl4-d5-all-heads", "wl4-d5-split", "wl5-d5",
         "wl5-d5-fused"])
 def test_full_size_workloads_sampled(wl, delta, heads, kernels):
     """Workloads 3-5 at full size in the benchmark's launch configuration (automatic splits);
