@@ -13,8 +13,9 @@ using namespace ffd;
 
 namespace {
 
-// Compute units of the current device, queried once per device and cached (the only state the
-// library keeps). kFallbackCus (an MI355X's count) is used if the query fails.
+// Compute units of the current device, queried once per device and cached (with the no-alloc
+// entry point's per-device scratch address below, the only state the library keeps). kFallbackCus
+// (an MI355X's count) is used if the query fails.
 constexpr int kFallbackCus = 256;
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];
