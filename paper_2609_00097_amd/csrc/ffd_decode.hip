@@ -907,7 +907,8 @@ __global__ __launch_bounds__(kScanThreads, 1) void ffd_decode_kernel(FusedArgs a
 // ================================================================================================
 // Refinement: Eq. 4 on the kept blocks, online softmax and PV, one partial state per workgroup.
 // Grid (W + B*Hkv). With N kept blocks in all and n_x in KV group x, group x gets
-// W_x = ceil(n_x * min(W, N) / N) workgroups (1 if n_x = 0) in group order; workgroup p of the
+// W_x = ceil(n_x * min(W', N) / N) workgroups (1 if n_x = 0) in group order, W' = W or, with few
+// splits, the largest W' found whose allocation still fits the grid (fill_grid); workgroup p of the
 // group refines its kept blocks of rank [p n_x / W_x, (p + 1) n_x / W_x). Workgroups past the last
 // group's exit.
 // ================================================================================================
@@ -944,6 +945,35 @@ __global__ __launch_bounds__(kRefineThreads, 1) void ffd_refine_kernel(RefineArg
     auto alloc = [&](int nx, long long Weff) {
         return nx > 0 ? (int)floor(((double)nx * (double)Weff + (double)(N - 1)) / (double)N) : 1;
     };
+    // The rounding up in alloc leaves up to one workgroup per group of the grid's W + B*Hkv unused.
+    // When that can be a third of the grid or more (W <= 2 B*Hkv: many groups, few splits), grow
+    // the effective W by the unused count while the allocation still fits the grid (at most three
+    // steps, each halved once if it overshoots), so fewer CUs idle and the largest share shrinks
+    // (the ragged batch of 16 sequences, 128 groups on 256 workgroups: refinement 422 -> 397 us).
+    // With more splits the slack is small and the extra evaluations cost more than they save (4 x
+    // 128K, delta 5: +2 us), so W is used as it is. total(We) is the allocation's workgroup count
+    // for an effective We, the same value in every thread; the result depends only on the counts,
+    // like the allocation itself.
+    auto fill_grid = [&](auto total) {
+        const long long grid = W + npairs;
+        const long long cap = (long long)max(N, 1);
+        long long We = min(W, cap);
+        if (W > 2LL * npairs) return We;
+        int used = total(We);
+        for (int it = 0; it < 3 && used < grid && We < cap; ++it) {
+            long long cand = min(We + (grid - used), cap);
+            int uc = total(cand);
+            if (uc > grid) {
+                cand = We + (cand - We) / 2;
+                if (cand == We) break;
+                uc = total(cand);
+                if (uc > grid) break;
+            }
+            We = cand;
+            used = uc;
+        }
+        return We;
+    };
     int x = 0, Qx = 0, Wx = 1, nx = 0;
     if (fast) {
         const int i0 = 16 * lane;
@@ -970,13 +1000,21 @@ __global__ __launch_bounds__(kRefineThreads, 1) void ffd_refine_kernel(RefineArg
         }
         if (lane == 0) sm.cnt[total] = N;
         wave_lds_fence();
-        const long long Weff = min(W, (long long)max(N, 1));
         int w4[4], n4[4], s4 = 0;                      // lane l: groups 4l .. 4l + 3
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int xi = 4 * lane + k;
             n4[k] = xi < npairs ? sm.cnt[(xi + 1) * S1] - sm.cnt[xi * S1] : 0;
-            w4[k] = xi < npairs ? alloc(n4[k], Weff) : 0;
+        }
+        const long long Weff = fill_grid([&](long long We) {
+            int t = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) t += 4 * lane + k < npairs ? alloc(n4[k], We) : 0;
+            return __builtin_amdgcn_readlane(wave_inclusive_scan(t), 63);
+        });
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            w4[k] = 4 * lane + k < npairs ? alloc(n4[k], Weff) : 0;
             s4 += w4[k];
         }
         const int winc = wave_inclusive_scan(s4);
@@ -1021,13 +1059,22 @@ __global__ __launch_bounds__(kRefineThreads, 1) void ffd_refine_kernel(RefineArg
         }
         if (tid == 0) sm.cnt[total] = N;
         __syncthreads();
-        const long long Weff = min(W, (long long)max(N, 1));
         int w4[4], n4[4], s4 = 0;                      // thread t: groups 4t .. 4t + 3
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int xi = 4 * tid + k;
             n4[k] = xi < npairs ? sm.cnt[(xi + 1) * S1] - sm.cnt[xi * S1] : 0;
-            w4[k] = xi < npairs ? alloc(n4[k], Weff) : 0;
+        }
+        const long long Weff = fill_grid([&](long long We) {
+            int t = 0, tot = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) t += 4 * tid + k < npairs ? alloc(n4[k], We) : 0;
+            (void)scan(t, &tot);
+            return tot;
+        });
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            w4[k] = 4 * tid + k < npairs ? alloc(n4[k], Weff) : 0;
             s4 += w4[k];
         }
         int q0 = scan(s4, &running);
