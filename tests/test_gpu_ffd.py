@@ -282,6 +282,22 @@ def test_allocation_for_more_than_1024_kv_groups():
     compare_ffd(c, 5.0, out, lse, mask)
 
 
+@pytest.mark.parametrize("B", [200, 300])
+def test_allocation_fills_the_grid_with_many_groups(B):
+    """Many KV groups and one refinement split (W <= 2 B*Hkv): the allocation grows its effective W
+    until the grid is full, in the per-wave allocation (200 groups) and in the LDS-cached one (300
+    groups); ragged lengths, empty sequences among them, both through the oracle."""
+    from paper_2609_00097_amd import ffd
+    lens = [0 if b % 37 == 5 else 1 + (97 * b) % 2000 for b in range(B)]
+    c = I.small_case(seed=71 + B, B=B, Hq=4, Hkv=1, seq_lens=lens, Lcap=2048, heavy_frac=0.03)
+    assert ffd.resolve_splits(B, 1, 2048, 0) == 1
+    print(f"case {B} groups, one refinement split", flush=True)
+    up = Uploaded(c)
+    qk = _quant(up)
+    out, lse, mask = _ffd(up, qk, 5.0, kernels="split")
+    compare_ffd(c, 5.0, out, lse, mask)
+
+
 def test_share_longer_than_the_per_wave_staging():
     """One split: a single refinement workgroup refines all 1094 kept blocks of the group, staged in
     two chunks with workgroup barriers (shares of up to 256 blocks are staged by each wave alone)."""
