@@ -114,6 +114,24 @@ def test_zero_keys_and_short_sequences(kernels, num_splits):
     assert not mask.cpu().numpy()[2].any()
 
 
+@pytest.mark.parametrize("kernels", KERNELS)
+def test_zero_queries(kernels):
+    """All-zero queries: every score is 0, so m~ = 0, every block ties it and is kept, and the output
+    is the mean of the values. Two heads of sequence 0 and every head of sequence 1 are zero."""
+    c = I.small_case(seed=79, B=2, Hq=8, Hkv=2, seq_lens=(700, 1500), Lcap=1536)
+    c.q[0, 0:2] = 0
+    c.q[1] = 0
+    up = Uploaded(c)
+    out, lse, mask = _ffd(up, _quant(up), 5.0, kernels=kernels)
+    compare_ffd(c, 5.0, out, lse, mask)
+    m = mask.cpu().numpy()
+    assert m[1, :, :(1500 + 63) // 64].all() and m[0, 0:2, :(700 + 63) // 64].all()
+    v = bf16_to_f64(up.v)
+    o = bf16_to_f64(out)
+    check_close("zero-query output", o[1], np.repeat(v[1, :, :1500].mean(axis=1), c.G, axis=0))
+    assert np.allclose(lse.cpu().numpy()[1], np.log(1500.0), atol=1e-3)
+
+
 def test_split_count_invariance():
     """Both kernel paths at several split counts give the same mask and, to rounding, the same
     outputs (the fused kernel with one split writes its outputs directly, without the merge)."""
