@@ -164,8 +164,9 @@ int ffd_decode_attention(const void* q, const void* k_codes, const void* k_absma
 
 /* Kernels of the top-delta rule (ffd_decode_extras.kernels). */
 #define FFD_KERNELS_AUTO 0    /* FFD_KERNELS_FUSED while each of its workgroups covers at most 64 blocks
-                                 of the capacity, or a sequence fits one workgroup (ffd_select_kernels),
-                                 else FFD_KERNELS_SPLIT */
+                                 of the capacity (128 when there is at most one workgroup per compute
+                                 unit), or a sequence fits one workgroup (ffd_select_kernels), else
+                                 FFD_KERNELS_SPLIT */
 #define FFD_KERNELS_FUSED 1   /* one kernel: each of S1 = ffd_fused_splits(...) workgroups per
                                  (sequence, KV head) scans the blocks j = s + S1 i, decides, refines and
                                  attends its own kept blocks; then the merge of the S1 partial states
@@ -257,8 +258,10 @@ int ffd_resolve_splits(int B, int Hkv, int Lcap, int num_splits);
 
 /* Workgroups per (sequence, KV head) of the fused top-delta kernel for this num_splits: num_splits
  * itself, or automatically 1 when the capacity has at most 64 blocks, else about 16 blocks of the
- * capacity per workgroup with at most two workgroups per compute unit in all; raised to
- * ceil((Lcap / 64) / 256) when smaller (a workgroup covers at most 256 blocks). 0 on invalid input. */
+ * capacity per workgroup with at most two workgroups per compute unit in all, or one per compute
+ * unit when that cap would leave 64 or more blocks per workgroup and one per unit leaves at most
+ * 128; raised to ceil((Lcap / 64) / 256) when smaller (a workgroup covers at most 256 blocks).
+ * 0 on invalid input. */
 int ffd_fused_splits(int B, int Hkv, int Lcap, int num_splits);
 
 /* The kernels FFD_KERNELS_AUTO uses for these arguments: FFD_KERNELS_FUSED or FFD_KERNELS_SPLIT;

@@ -154,6 +154,8 @@ int scan_splits(int B, int Hkv, int Lcap) {
 // 16K 14.6 (16), 32K 15.7 (16..32), 64K 25.0 (64), 128K 29.8 (64).
 constexpr int kFusedAloneBlocks = 64;
 constexpr int kFusedTargetBlocks = 16;
+constexpr int kFusedMaxBlocks = 64;            // blocks per workgroup the fused kernel takes ...
+constexpr int kFusedWideMaxBlocks = 128;       // ... or this many with at most one workgroup per CU
 
 int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
     if (B <= 0 || Hkv <= 0 || Lcap <= 0 || num_splits < 0 || num_splits > FFD_MAX_SPLITS) return 0;
@@ -167,7 +169,19 @@ int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
         } else {
             s = (nblk_cap + kFusedTargetBlocks - 1) / kFusedTargetBlocks;
             const long long cap = 2LL * device_cus() / pairs;
-            if (s > cap) s = cap;
+            if (s > cap) {
+                s = cap;
+                // where the two-per-CU cap leaves kFusedMaxBlocks or more blocks per workgroup, one
+                // workgroup per CU with up to twice the blocks streams better (its waves do not
+                // queue behind another workgroup's on the CU): at 1 x 256K, 32q/8kv, delta 5, 32
+                // workgroups of 128 blocks per group 31.1 us (the clustered workload: 29.6 us)
+                // against 32.7 (31.6) us for 64 of 64 blocks; at 1 x 128K the 64 workgroups of 32
+                // blocks stay ahead (29.5 against 34.0 us)
+                const long long one = std::max(1LL, (long long)device_cus() / pairs);
+                if (s > 0 && (nblk_cap + s - 1) / s >= kFusedMaxBlocks &&
+                    (nblk_cap + one - 1) / one <= kFusedWideMaxBlocks)
+                    s = one;
+            }
         }
     }
     if (s < need) s = need;
@@ -181,13 +195,14 @@ int decode_splits(int B, int Hkv, int Lcap, int num_splits) {
 // refinement + merge, whose refinement spreads the kept blocks over every CU. (The fused kernel
 // refines each workgroup's own kept blocks, so its time follows the workgroup with the most: at
 // 4 x 128K, 32q/8kv, delta 5, its best split count gave 66.9 us against 58.9 us for the split
-// kernels; at 1 x 256K, 64 workgroups of 64 blocks per group gave 32.4 us against 34.1 us.)
-constexpr int kFusedMaxBlocks = 64;
-
-int auto_kernels(int Lcap, int S1f) {
+// kernels; at 1 x 256K, 32 workgroups of 128 blocks per group gave 31.1 us against 34.3 us.) With
+// at most one workgroup per CU the fused kernel takes up to kFusedWideMaxBlocks blocks each.
+int auto_kernels(int B, int Hkv, int Lcap, int S1f) {
     const int nblk_cap = Lcap / FFD_BLOCK;
     const int bps = (nblk_cap + S1f - 1) / S1f;
-    return bps <= kFusedMaxBlocks || nblk_cap <= kFusedAloneBlocks ? FFD_KERNELS_FUSED : FFD_KERNELS_SPLIT;
+    const bool one_per_cu = (long long)S1f * B * Hkv <= device_cus();
+    return bps <= kFusedMaxBlocks || nblk_cap <= kFusedAloneBlocks || (one_per_cu && bps <= kFusedWideMaxBlocks)
+               ? FFD_KERNELS_FUSED : FFD_KERNELS_SPLIT;
 }
 
 // FFD workspace: partial states (for the fused top-delta kernel's B * Hq * S1f rows, or for the
@@ -327,7 +342,7 @@ int ffd_fused_splits(int B, int Hkv, int Lcap, int num_splits) {
 int ffd_select_kernels(int B, int Hkv, int Lcap, int num_splits) {
     const int S1f = decode_splits(B, Hkv, Lcap, num_splits);
     if (S1f <= 0) return 0;
-    return auto_kernels(Lcap, S1f);
+    return auto_kernels(B, Hkv, Lcap, S1f);
 }
 
 int ffd_dense_resolve_splits(int B, int Hkv, int Lcap, int num_splits) {
@@ -462,7 +477,7 @@ int ffd_decode_attention_ex(const void* q, const void* k_codes, const void* k_ab
 
     const int mode = top_k > 0 ? kSelTopK : (pm_source == FFD_PSEUDO_MAX_REFINED ? kSelRefinedPM : kSelThumbnailPM);
     if ((st = mark(0)) != FFD_OK) return st;
-    const int kernels = kernels_req == FFD_KERNELS_AUTO ? auto_kernels(Lcap, S1f) : kernels_req;
+    const int kernels = kernels_req == FFD_KERNELS_AUTO ? auto_kernels(B, Hkv, Lcap, S1f) : kernels_req;
     if (top_k == 0 && kernels == FFD_KERNELS_FUSED) {
         // top-delta, fused: one kernel, then the merge of its S1f partial states per head (none when
         // S1f == 1: the kernel writes the outputs itself)

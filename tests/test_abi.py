@@ -55,6 +55,8 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_fused_splits(1, 2, 4096, 0) == 1                # 64 blocks: one workgroup, no merge
     assert so.ffd_fused_splits(1, 8, 8192, 0) == 8                # 128 blocks / 16
     assert so.ffd_fused_splits(1, 8, 131072, 0) == 64             # capped: 512 / 8 groups
+    assert so.ffd_fused_splits(1, 8, 262144, 0) == 32             # 512 / 8 leaves 64 blocks: one per CU
+    assert so.ffd_fused_splits(2, 8, 131072, 0) == 16             # 512 / 16 leaves 64 blocks: one per CU
     assert so.ffd_fused_splits(4, 8, 131072, 0) == 16             # capped: 512 / 32 groups
     assert so.ffd_fused_splits(4, 6, 131072, 0) == 21             # floor(512 / 24)
     assert so.ffd_fused_splits(64, 8, 131072, 0) == 8             # at least 2048 / 256
@@ -66,7 +68,8 @@ def test_splits_and_workspace_sizes(so):
     assert so.ffd_select_kernels(1, 2, 4096, 0) == 1
     assert so.ffd_select_kernels(1, 8, 32768, 0) == 1             # 32 workgroups of 16 blocks
     assert so.ffd_select_kernels(1, 8, 131072, 0) == 1            # 64 workgroups of 32 blocks
-    assert so.ffd_select_kernels(1, 8, 262144, 0) == 1            # 64 blocks per workgroup
+    assert so.ffd_select_kernels(1, 8, 262144, 0) == 1            # 128 blocks, one workgroup per CU
+    assert so.ffd_select_kernels(2, 8, 131072, 0) == 1            # 128 blocks, one workgroup per CU
     assert so.ffd_select_kernels(1, 8, 524288, 0) == 2            # 128 blocks per workgroup
     assert so.ffd_select_kernels(4, 8, 131072, 0) == 2            # 128 blocks per workgroup
     assert so.ffd_select_kernels(4, 8, 131072, 32) == 1           # 64 blocks per workgroup
