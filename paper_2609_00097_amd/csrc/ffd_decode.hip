@@ -940,8 +940,9 @@ __global__ __launch_bounds__(kRefineThreads, 1) void ffd_refine_kernel(RefineArg
         return e;
     };
     const long long W = a.W;
-    // ceil(n_x * min(W, N) / N) workgroups for n_x > 0; exact in fp64 (the numerator stays below
-    // 2^52, and fl(u / N) cannot round up to an integer when u < 2^52)
+    // ceil(n_x * We / N) workgroups for n_x > 0, We = min(W, N) or the grid-filling W' below; exact
+    // in fp64 (the numerator stays below 2^52, and fl(u / N) cannot round up to an integer when
+    // u < 2^52)
     auto alloc = [&](int nx, long long Weff) {
         return nx > 0 ? (int)floor(((double)nx * (double)Weff + (double)(N - 1)) / (double)N) : 1;
     };

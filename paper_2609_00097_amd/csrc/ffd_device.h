@@ -125,10 +125,11 @@ __device__ __forceinline__ int wg_exclusive_scan(int x, int* wsum, int* total) {
     return before + incl - x;
 }
 
-// Work decomposition shared by both attention kernels: a workgroup of 4 waves serves one
-// (sequence, KV head, split); wave w owns tokens [16w, 16w + 16) of every 64-token block of the
-// split (one MFMA tile), so each wave keeps its own online-softmax state over its tiles and the
-// four states are merged in the epilogue.
+// Work decomposition of the attention kernels: wave w owns tokens [16 (w mod 4), 16 (w mod 4) + 16)
+// (one MFMA tile) of the 64-token blocks it handles. The dense kernel's 4-wave workgroups take every
+// block of their run; the FFD kernels' 8-wave workgroups give waves w and w + 4 alternate kept
+// blocks. Each wave keeps its own online-softmax state over its tiles, and the workgroup's states
+// are merged in the epilogue.
 
 // PV accumulators of one wave for 4 * NT heads: lane l holds dims 2l and 2l + 1 of every head;
 // acc[h][e] is the unnormalised sum of p * v.
